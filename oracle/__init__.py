@@ -1,0 +1,374 @@
+"""CPU oracle for the Reflective Verification verify pass -- TEST INFRASTRUCTURE.
+
+Only tests/, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package. It shares no code with the GPU library
+and never imports it.
+
+What it computes (arXiv 2505.18629):
+  * Section 3.1, Eq. 1 and Algorithm 1: the reflective draft is
+    [x_1..x_g, template, x_1..x_g] with template = probe || prefix-position
+    tokens, scored in one causal forward pass after the prefix.
+  * Algorithm 1: original logits o_1..o_{g+1} and reflective logits
+    o_m..o_{m+g} with m = g + |template| + 1.
+  * Section 3.2, Eq. 2: p_i = softmax((1 - alpha) * o_i + alpha * r_i).
+  * Appendix A, Algorithm 2 (exact-match verification), at temperature 0.
+
+Because one causal pass produces exactly the next-token logits at every block
+position, the oracle is that definition written out: a plain Llama-style
+decoder run from scratch over prefix || block (no KV cache), then the rows
+Algorithm 1 names are picked out, fused and verified.
+
+Precision modes:
+  "exact"    -- fp64 everywhere (used to pin the decoder against a library
+                implementation);
+  "contract" -- fp64 arithmetic, but values are rounded at the points where
+                the GPU library stores them: fp32 for every matmul result and
+                the residual stream, the storage dtype (bf16 or fp32) for the
+                matmul operands, q/k/v after rotary and the attention output.
+                The only remaining GPU-vs-oracle differences are fp32
+                accumulation order.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Dict, List, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle_weights.so")
+_lib = None
+
+
+def build() -> str:
+    """Compile the weight generator (plain C, OpenMP)."""
+    src = os.path.join(_HERE, "weights.c")
+    cmd = ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c11", src, "-o", _LIB_PATH, "-lm"]
+    subprocess.run(cmd, check=True)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        u64, i64, dbl = ctypes.c_uint64, ctypes.c_int64, ctypes.c_double
+        vp = ctypes.c_void_p
+        lib.orc_fill.argtypes = [u64, u64, u64, u64, ctypes.c_int, dbl, vp]
+        lib.orc_fill.restype = None
+        lib.orc_bits_at.argtypes = [u64, u64, vp, i64, ctypes.c_int, dbl, vp]
+        lib.orc_bits_at.restype = None
+        lib.orc_splitmix64_stream.argtypes = [u64, ctypes.c_int, vp]
+        lib.orc_splitmix64_stream.restype = None
+        lib.orc_round_bf16.argtypes = [vp, vp, i64]
+        lib.orc_round_bf16.restype = None
+        lib.orc_scale.argtypes = [dbl]
+        lib.orc_scale.restype = ctypes.c_float
+        _lib = lib
+    return _lib
+
+
+# ---------------------------------------------------------------- weights
+
+TENSOR_NAMES = ("q", "k", "v", "o", "gate", "up", "down")
+
+
+def tensor_index(shape, layer: int | None, name: str) -> int:
+    """Generator tensor numbering: 0 embedding, 1 + 7l + j per layer matrix,
+    1 + 7L the LM head."""
+    if name == "embed":
+        return 0
+    if name == "lm_head":
+        return 1 + 7 * shape.n_layers
+    return 1 + 7 * layer + TENSOR_NAMES.index(name)
+
+
+def tensor_dims(shape, name: str):
+    """Logical [out][in] dims of a weight matrix (y = x @ W.T)."""
+    d, hd, F, V = shape.d_model, shape.head_dim, shape.ffn_dim, shape.vocab
+    qd, kvd = shape.n_heads * hd, shape.n_kv_heads * hd
+    return {
+        "embed": (V, d), "lm_head": (V, d),
+        "q": (qd, d), "k": (kvd, d), "v": (kvd, d), "o": (d, qd),
+        "gate": (F, d), "up": (F, d), "down": (d, F),
+    }[name]
+
+
+def _is_bf16(shape) -> int:
+    return 1 if shape.dtype == "bf16" else 0
+
+
+def fill(shape, seed: int, t: int, start: int, count: int) -> np.ndarray:
+    out = np.empty(count, dtype=np.float64)
+    _load().orc_fill(seed, t, start, count, _is_bf16(shape), shape.init_std,
+                     out.ctypes.data_as(ctypes.c_void_p))
+    return out
+
+
+def weight(shape, seed: int, layer: int | None, name: str, row0: int = 0, nrows: int | None = None) -> np.ndarray:
+    """Rows [row0, row0 + nrows) of a logical weight matrix, as fp64."""
+    n_out, n_in = tensor_dims(shape, name)
+    if nrows is None:
+        nrows = n_out - row0
+    t = tensor_index(shape, layer, name)
+    return fill(shape, seed, t, row0 * n_in, nrows * n_in).reshape(nrows, n_in)
+
+
+def weight_bits(shape, seed: int, layer: int | None, name: str, flat_idx: np.ndarray) -> np.ndarray:
+    """Stored bit patterns (bf16 in the low 16 bits, or fp32) at flat logical indices."""
+    idx = np.ascontiguousarray(flat_idx, dtype=np.uint64)
+    out = np.empty(len(idx), dtype=np.uint32)
+    _load().orc_bits_at(seed, tensor_index(shape, layer, name), idx.ctypes.data_as(ctypes.c_void_p),
+                        len(idx), _is_bf16(shape), shape.init_std, out.ctypes.data_as(ctypes.c_void_p))
+    return out
+
+
+def embedding_rows(shape, seed: int, tokens: Sequence[int]) -> np.ndarray:
+    d = shape.d_model
+    out = np.empty((len(tokens), d), dtype=np.float64)
+    cache: Dict[int, np.ndarray] = {}
+    for j, tok in enumerate(tokens):
+        tok = int(tok)
+        if tok not in cache:
+            cache[tok] = fill(shape, seed, 0, tok * d, d)
+        out[j] = cache[tok]
+    return out
+
+
+def splitmix64_stream(seed: int, n: int) -> List[int]:
+    out = np.empty(n, dtype=np.uint64)
+    _load().orc_splitmix64_stream(seed, n, out.ctypes.data_as(ctypes.c_void_p))
+    return [int(v) for v in out]
+
+
+# ---------------------------------------------------------------- rounding
+
+def round_f32(x: np.ndarray) -> np.ndarray:
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round through fp32 to bf16, nearest-even at each step."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    out = np.empty_like(x)
+    _load().orc_round_bf16(x.ctypes.data_as(ctypes.c_void_p), out.ctypes.data_as(ctypes.c_void_p), x.size)
+    return out
+
+
+class _Rounding:
+    def __init__(self, shape, mode: str):
+        if mode not in ("exact", "contract"):
+            raise ValueError(mode)
+        self.exact = mode == "exact"
+        self.bf16 = shape.dtype == "bf16"
+
+    def f32(self, x):
+        return x if self.exact else round_f32(x)
+
+    def store(self, x):
+        """Rounding to the storage dtype (matmul operands, q/k/v, attention out)."""
+        if self.exact:
+            return x
+        return round_bf16(x) if self.bf16 else round_f32(x)
+
+
+# ---------------------------------------------------------------- decoder
+
+def rms_norm(h: np.ndarray, eps: float) -> np.ndarray:
+    """y = h / sqrt(mean(h^2) + eps) * g, with gains g = 1 at init."""
+    return h / np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + eps)
+
+
+def rope_table(shape, positions: np.ndarray, rnd: _Rounding):
+    """cos/sin of p * base^(-2i/hd), i < hd/2, evaluated in fp64; the contract
+    stores the table in fp32."""
+    hd = shape.head_dim
+    i = np.arange(hd // 2, dtype=np.float64)
+    theta = shape.rope_base ** (-2.0 * i / hd)
+    ang = np.asarray(positions, dtype=np.float64)[:, None] * theta[None, :]
+    return rnd.f32(np.cos(ang)), rnd.f32(np.sin(ang))
+
+
+def rope(x: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
+    """Rotate-half rotary embedding: dims (i, i + hd/2) rotate by angle_i.
+    x is [n][heads][hd]; cos/sin are [n][hd/2]."""
+    half = x.shape[-1] // 2
+    x1, x2 = x[..., :half], x[..., half:]
+    c, s = cos[:, None, :], sin[:, None, :]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
+
+
+def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """Softmax(q k^T / sqrt(hd)) v with row j attending keys 0..j; q head h
+    reads kv head h // (Hq / Hkv). q [n][Hq][hd], k/v [n][Hkv][hd]."""
+    n, Hq, hd = q.shape
+    group = Hq // k.shape[1]
+    out = np.empty_like(q)
+    mask = np.triu(np.ones((n, n), dtype=bool), k=1)
+    for h in range(Hq):
+        kv = h // group
+        s = (q[:, h, :] @ k[:, kv, :].T) / np.sqrt(hd)
+        s[mask] = -np.inf
+        s = s - s.max(axis=1, keepdims=True)
+        p = np.exp(s)
+        p /= p.sum(axis=1, keepdims=True)
+        out[:, h, :] = p @ v[:, kv, :]
+    return out
+
+
+def silu(x: np.ndarray) -> np.ndarray:
+    return x / (1.0 + np.exp(-x))
+
+
+def _matmul_wT(shape, seed, layer, name, a, rnd: _Rounding, chunk_rows: int = 16384):
+    """a @ W.T, W generated in row chunks to bound memory; fp32-rounded in the contract."""
+    n_out, _ = tensor_dims(shape, name)
+    if n_out <= chunk_rows:
+        return rnd.f32(a @ weight(shape, seed, layer, name).T)
+    parts = []
+    for r0 in range(0, n_out, chunk_rows):
+        nr = min(chunk_rows, n_out - r0)
+        parts.append(a @ weight(shape, seed, layer, name, r0, nr).T)
+    return rnd.f32(np.concatenate(parts, axis=1))
+
+
+def forward(shape, seed: int, tokens: Sequence[int], rows: Sequence[int], mode: str = "contract",
+            return_kv: bool = False):
+    """Next-token logits at the given rows of `tokens`, computed from scratch.
+
+    Returns logits [len(rows)][V] (fp64 holding fp32 values in the contract
+    mode) and, if asked, the per-layer K and V caches [L][n][Hkv][hd] as the
+    GPU stores them (post-rotary, storage dtype)."""
+    rnd = _Rounding(shape, mode)
+    tokens = np.asarray(tokens, dtype=np.int64)
+    n = len(tokens)
+    Hq, Hkv, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
+    cos, sin = rope_table(shape, np.arange(n), rnd)
+    h = embedding_rows(shape, seed, tokens)
+    ks, vs = [], []
+    for l in range(shape.n_layers):
+        a = rnd.store(rms_norm(h, shape.rms_eps))
+        q = _matmul_wT(shape, seed, l, "q", a, rnd).reshape(n, Hq, hd)
+        k = _matmul_wT(shape, seed, l, "k", a, rnd).reshape(n, Hkv, hd)
+        v = _matmul_wT(shape, seed, l, "v", a, rnd).reshape(n, Hkv, hd)
+        q = rnd.store(rope(q, cos, sin))
+        k = rnd.store(rope(k, cos, sin))
+        v = rnd.store(v)
+        if return_kv:
+            ks.append(k)
+            vs.append(v)
+        att = rnd.store(causal_attention(q, k, v).reshape(n, Hq * hd))
+        h = rnd.f32(h + _matmul_wT(shape, seed, l, "o", att, rnd))
+        a = rnd.store(rms_norm(h, shape.rms_eps))
+        g = _matmul_wT(shape, seed, l, "gate", a, rnd)
+        u = _matmul_wT(shape, seed, l, "up", a, rnd)
+        act = rnd.store(silu(g) * u)
+        h = rnd.f32(h + _matmul_wT(shape, seed, l, "down", act, rnd))
+    rows = np.asarray(rows, dtype=np.int64)
+    a = rnd.store(rms_norm(h[rows], shape.rms_eps))
+    logits = _matmul_wT(shape, seed, None, "lm_head", a, rnd)
+    if return_kv:
+        return logits, np.stack(ks), np.stack(vs)
+    return logits
+
+
+# ---------------------------------------------------------------- the method
+
+def reflective_block(history: Sequence[int], drafts: Sequence[int], probe: Sequence[int], prefix_pos: int):
+    """Block scored by one verify pass (Eq. 1; Algorithm 1).
+
+    Row 0 is the last committed token c = history[-1], whose KV is not cached
+    yet (it was emitted as the previous step's bonus token); it yields o_1.
+    The reflective draft [x, probe, history[-P:], x] follows.  shift is the
+    number of tokens of the probe, the prefix-position part and the first draft
+    copy (Eq. 2's shift_len), so r_i sits at block row shift + i - 1.
+    """
+    L, k, P = len(history), len(drafts), prefix_pos
+    if P > L:
+        raise ValueError("prefix_pos exceeds the committed length")
+    template = list(probe) + (list(history[L - P:]) if P > 0 else [])
+    block = [int(history[-1])] + list(drafts) + template + list(drafts)
+    shift = k + len(template)
+    orig_rows = list(range(k + 1))
+    refl_rows = [shift + i for i in range(k + 1)]
+    return [int(t) for t in block], shift, orig_rows, refl_rows
+
+
+def fuse(o: np.ndarray, r: np.ndarray, alpha: float) -> np.ndarray:
+    """Eq. 2's fused logits, in fp32: (1 - alpha) * o + alpha * r."""
+    a = np.float32(alpha)
+    return (np.float32(1.0) - a) * np.asarray(o, np.float32) + a * np.asarray(r, np.float32)
+
+
+def log_softmax(x: np.ndarray) -> np.ndarray:
+    x = np.asarray(x, dtype=np.float64)
+    m = x.max(axis=-1, keepdims=True)
+    return x - (m + np.log(np.exp(x - m).sum(axis=-1, keepdims=True)))
+
+
+def accept_greedy(z: np.ndarray, drafts: Sequence[int]):
+    """Algorithm 2 at temperature 0: x_hat_i = argmax p_i (lowest id on ties);
+    n = number of leading drafts equal to x_hat; t = argmax p_{n+1}."""
+    k = len(drafts)
+    xhat = np.argmax(z, axis=-1)
+    n = k
+    for i in range(k):
+        if int(xhat[i]) != int(drafts[i]):
+            n = i
+            break
+    return n, int(xhat[n])
+
+
+def decision_margins(z: np.ndarray, drafts: Sequence[int], n: int, tie_eps: float = 1e-3):
+    """Distance of each decision on the accept path from its boundary, in
+    fused-logit units: z_i[x_i] - max_{v != x_i} z_i[v] for the drafts that
+    were tested, and top1 - top2 of z_{n+1} for the bonus token."""
+    k = len(drafts)
+    ms = []
+    for i in range(min(n + 1, k)):
+        zi = np.asarray(z[i], dtype=np.float64)
+        x = int(drafts[i])
+        others = np.delete(zi, x)
+        ms.append(float(zi[x] - others.max()))
+    top = np.sort(np.asarray(z[n], dtype=np.float64))[-2:]
+    gap = float(top[1] - top[0])
+    near = any(abs(m) < tie_eps for m in ms) or gap < tie_eps
+    return ms, gap, near
+
+
+def verify(shape, seed: int, history: Sequence[int], drafts: Sequence[int], probe: Sequence[int],
+           alpha: float, prefix_pos: int, mode: str = "contract") -> Dict:
+    """One verify step for one sequence (Algorithm 1 with Algorithm 2's rule)."""
+    history = [int(t) for t in history]
+    drafts = [int(t) for t in drafts]
+    block, shift, orig_rows, refl_rows = reflective_block(history, drafts, probe, prefix_pos)
+    base = len(history) - 1
+    seq = history[:-1] + block
+    rows = [base + j for j in orig_rows] + [base + j for j in refl_rows]
+    logits = forward(shape, seed, seq, rows, mode)
+    k = len(drafts)
+    o, r = logits[: k + 1], logits[k + 1:]
+    z = fuse(o, r, alpha)
+    n, t = accept_greedy(z, drafts)
+    ms, gap, near = decision_margins(z, drafts, n)
+    return {
+        "block": block, "shift": shift, "o": o, "r": r, "z": z.astype(np.float64),
+        "lp_o": log_softmax(o), "lp_r": log_softmax(r), "lp_z": log_softmax(z),
+        "accept_len": n, "next_id": t, "margins": ms, "gap": gap, "near_tie": near,
+    }
+
+
+def greedy_continuation(shape, seed: int, history: Sequence[int], n_tokens: int, mode: str = "contract") -> List[int]:
+    """Target's own greedy continuation (used to build realistic drafts)."""
+    seq = [int(t) for t in history]
+    out = []
+    for _ in range(n_tokens):
+        logits = forward(shape, seed, seq, [len(seq) - 1], mode)
+        t = int(np.argmax(logits[0]))
+        out.append(t)
+        seq.append(t)
+    return out

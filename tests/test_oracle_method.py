@@ -1,0 +1,136 @@
+"""Pins of the oracle's method steps (CPU only): block construction (Eq. 1,
+Algorithm 1), fusion (Eq. 2), the exact-match rule (Algorithm 2), and the
+single-pass claim checked by brute-force token-by-token decoding."""
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+
+import oracle
+import workload
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def load(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def test_block_layout_golden():
+    g = load("block_layout.json")
+    block, shift, orig, refl = oracle.reflective_block(g["history"], g["drafts"], g["probe"], g["prefix_pos"])
+    assert block == g["expected_block"]
+    assert len(block) - 1 == g["expected_reflective_tokens"]  # row 0 is the pending committed token
+    assert shift == g["expected_shift"]
+    # Algorithm 1's m is 1-indexed over [c, reflective_draft] outputs: o_m sits at block row m - 1
+    assert shift == g["expected_m"] - 1
+    assert orig == g["expected_orig_rows"] and refl == g["expected_refl_rows"]
+    # the second copy is the same drafts, each predicted by the row before it
+    k = len(g["drafts"])
+    assert block[shift + 1: shift + 1 + k] == g["drafts"] == block[1: 1 + k]
+
+
+def test_block_degenerate_cases():
+    h = [5, 6, 7]
+    # empty probe (Table 2's empty-prompt variant) and P = 0 (Algorithm 1 literally)
+    block, shift, orig, refl = oracle.reflective_block(h, [1, 2], [], 0)
+    assert block == [7, 1, 2, 1, 2] and shift == 2 and refl == [2, 3, 4]
+    # k = 0: one greedy decode step, original and reflective rows coincide
+    block, shift, orig, refl = oracle.reflective_block(h, [], [], 0)
+    assert block == [7] and orig == [0] and refl == [0]
+    with pytest.raises(ValueError):
+        oracle.reflective_block(h, [1], [], 4)
+
+
+@pytest.mark.parametrize("case", load("accept_cases.json")["cases"], ids=lambda c: c["name"])
+def test_accept_rule_golden(case):
+    o = np.array(case["o"], dtype=np.float64)
+    r = np.array(case["r"], dtype=np.float64)
+    z = oracle.fuse(o, r, case["alpha"])
+    if "expected_z_row0" in case:
+        np.testing.assert_allclose(z[0], case["expected_z_row0"], atol=1e-6)
+    n, t = oracle.accept_greedy(z, case["drafts"])
+    assert (n, t) == (case["n"], case["t"])
+
+
+def test_fusion_end_points_and_shift_invariance():
+    rng = np.random.default_rng(0)
+    o = (rng.standard_normal((5, 300)) * 3).astype(np.float32).astype(np.float64)
+    r = (rng.standard_normal((5, 300)) * 3).astype(np.float32).astype(np.float64)
+    np.testing.assert_array_equal(oracle.fuse(o, r, 0.0), o.astype(np.float32))
+    np.testing.assert_array_equal(oracle.fuse(o, r, 1.0), r.astype(np.float32))
+    # fusing logits equals fusing log-probabilities (softmax shift invariance):
+    # p ~ p_o^(1-a) * p_r^a
+    a = 0.3
+    lp = oracle.log_softmax(oracle.fuse(o, r, a))
+    lp2 = scipy.special.log_softmax((1 - a) * scipy.special.log_softmax(o, axis=-1)
+                                    + a * scipy.special.log_softmax(r, axis=-1), axis=-1)
+    np.testing.assert_allclose(lp, lp2, atol=1e-5)
+    np.testing.assert_allclose(np.exp(lp).sum(-1), 1.0, atol=1e-12)
+    np.testing.assert_allclose(oracle.log_softmax(o), scipy.special.log_softmax(o, axis=-1), atol=1e-12)
+
+
+def test_margins_flag_near_ties():
+    z = np.array([[0.0, 1.0, 1.0005, 0.0], [2.0, 0.0, 0.0, 0.0]], dtype=np.float32)
+    n, t = oracle.accept_greedy(z, [2])
+    ms, gap, near = oracle.decision_margins(z, [2], n)
+    assert n == 1 and t == 0 and near and abs(ms[0] - 0.0005) < 1e-6
+    z2 = np.array([[0.0, 1.0, 1.5, 0.0], [2.0, 0.0, 0.0, 0.0]], dtype=np.float32)
+    assert not oracle.decision_margins(z2, [2], 1)[2]
+
+
+# ------------------------------------------------------------ on a tiny model
+
+SHAPE = workload.TINY
+SEED = 0
+
+
+@pytest.fixture(scope="module")
+def history():
+    return list(workload.random_ids(SHAPE.vocab, 40, 99, 0))
+
+
+def test_bruteforce_rows_equal_single_pass(history):
+    """Each o_i and r_i equals decoding the corresponding prefix from scratch."""
+    drafts = list(workload.random_ids(SHAPE.vocab, 3, 99, 1))
+    probe = list(workload.random_ids(SHAPE.vocab, 4, 99, 2))
+    P = 4
+    res = oracle.verify(SHAPE, SEED, history, drafts, probe, 0.3, P)
+    k = len(drafts)
+    for i in range(k + 1):
+        seq_o = history + drafts[:i]
+        lo = oracle.forward(SHAPE, SEED, seq_o, [len(seq_o) - 1])[0]
+        np.testing.assert_allclose(res["o"][i], lo, rtol=0, atol=1e-9)
+        seq_r = history + drafts + probe + history[-P:] + drafts[:i]
+        lr = oracle.forward(SHAPE, SEED, seq_r, [len(seq_r) - 1])[0]
+        np.testing.assert_allclose(res["r"][i], lr, rtol=0, atol=1e-9)
+
+
+def test_probe_does_not_change_original_rows(history):
+    drafts = list(workload.random_ids(SHAPE.vocab, 4, 98, 1))
+    a = oracle.verify(SHAPE, SEED, history, drafts, list(workload.random_ids(SHAPE.vocab, 5, 98, 2)), 0.3, 4)
+    b = oracle.verify(SHAPE, SEED, history, drafts, list(workload.random_ids(SHAPE.vocab, 5, 98, 3)), 0.3, 4)
+    np.testing.assert_allclose(a["o"], b["o"], atol=1e-9)
+    assert np.abs(a["r"] - b["r"]).max() > 1e-3
+
+
+def test_greedy_drafts_fully_accepted_at_alpha_zero(history):
+    g = oracle.greedy_continuation(SHAPE, SEED, history, 5)
+    res = oracle.verify(SHAPE, SEED, history, g[:4], [], 0.0, 0)
+    assert res["accept_len"] == 4 and res["next_id"] == g[4]
+    # k = 0 is a single greedy decode step
+    res0 = oracle.verify(SHAPE, SEED, history, [], [], 0.0, 0)
+    assert res0["accept_len"] == 0 and res0["next_id"] == g[0]
+
+
+def test_alpha_zero_is_standard_verification(history):
+    drafts = list(workload.corrupt(oracle.greedy_continuation(SHAPE, SEED, history, 4), 0.5, SHAPE.vocab,
+                                   np.random.default_rng(3)))
+    res = oracle.verify(SHAPE, SEED, history, drafts, list(workload.random_ids(SHAPE.vocab, 8, 3, 3)), 0.0, 4)
+    np.testing.assert_array_equal(res["z"], res["o"].astype(np.float32))
+    n, t = oracle.accept_greedy(res["o"], drafts)
+    assert (res["accept_len"], res["next_id"]) == (n, t)
+    np.testing.assert_allclose(np.exp(res["lp_z"]).sum(-1), 1.0, atol=1e-9)
