@@ -1,0 +1,207 @@
+/*
+ * rv.h -- C ABI of the MI355X (gfx950) Reflective Verification verify pass.
+ *
+ * Method: "Think Before You Accept: Semantic Reflective Verification for
+ * Faster Speculative Decoding" (arXiv 2505.18629).  One verify call scores,
+ * in a single causal forward pass of the target model, the block
+ *
+ *     [c, x_1..x_k, R, ids[L-P..L-1], x_1..x_k]                (Eq. 1)
+ *
+ * against the cached prefix, where c = ids[L-1] is the last committed token
+ * (its KV is not cached yet), x are the k draft tokens, R the reflective
+ * probe ids and ids[L-P..L-1] the prefix-position tokens (Section 3.1,
+ * Algorithm 1).  Block row i-1 gives the original logits o_i and block row
+ * shift+i-1 the reflective logits r_i (i = 1..k+1, shift = k + |R| + P).
+ * They are fused as z_i = (1 - alpha) o_i + alpha r_i (Eq. 2, Section 3.2),
+ * and the exact-match rule of Algorithm 2 (Appendix A) at temperature 0
+ * gives the accepted length n and the next token t = argmax z_{n+1}.
+ *
+ * Conventions
+ *  - Every device pointer is caller-owned device memory (e.g. a torch
+ *    tensor).  The library never allocates or frees device memory except
+ *    the small per-cache partial-sum region it carves out of the cache
+ *    buffer the caller provides.
+ *  - `stream` is a hipStream_t passed as void* (NULL = default stream).
+ *    Calls that take a stream are asynchronous on it; the library never
+ *    synchronises the device.
+ *  - Host pointers are prefixed h_, device pointers d_.
+ *  - Every function validates its arguments on the host first.  On any
+ *    validation failure it returns a negative rv_status and enqueues no
+ *    device work; rv_last_error() then describes the failure (thread-local).
+ *  - int32 token ids; ids outside [0, vocab) are detected on the device and
+ *    reported per sequence (accept_len = next_id = -1).
+ */
+#ifndef RV_H
+#define RV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RV_OK = 0,
+  RV_E_ARG = -1,      /* null pointer, bad enum, size or value out of its domain */
+  RV_E_RANGE = -2,    /* a prefix length outside [max(1, P), max_len] */
+  RV_E_CAPACITY = -3, /* block does not fit: L - 1 + S > max_len, or S > max_block */
+  RV_E_BUFFER = -4,   /* caller buffer smaller than the required byte count */
+  RV_E_HIP = -5,      /* a HIP runtime call or kernel launch failed */
+  RV_E_STATE = -6     /* handle used in a state that does not allow the call */
+} rv_status;
+
+enum { RV_F32 = 0, RV_BF16 = 1 };
+enum { RV_RULE_GREEDY = 0 };
+enum { RV_MAX_BATCH = 256, RV_MAX_DRAFTS = 32 };
+
+/* Decoder shape.  Llama-style: pre-norm RMSNorm, rotate-half rotary, GQA
+ * (query head h uses kv head h / (n_heads / n_kv_heads)), SwiGLU FFN,
+ * untied LM head, no biases.  dtype is the storage type of weights, matmul
+ * operands and the KV cache; accumulation is fp32.
+ * Requirements: d_model, ffn_dim % 32 == 0; head_dim % 16 == 0 and <= 128;
+ * n_heads % n_kv_heads == 0; vocab % 16 == 0. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  int32_t dtype;   /* RV_F32 or RV_BF16 */
+  float rms_eps;   /* RMSNorm epsilon, e.g. 1e-5 */
+  float rope_base; /* rotary base, e.g. 10000 */
+  float init_std;  /* std of the random-init weights, e.g. 0.02 */
+} rv_config;
+
+/* Fusion and verification parameters (Eq. 2, Table 5, Algorithm 2). */
+typedef struct {
+  float alpha;        /* weight of the reflective logits, 0 <= alpha <= 1 (Eq. 2) */
+  int32_t prefix_pos; /* P: committed tokens re-presented after the probe (Eq. 1) */
+  int32_t rule;       /* RV_RULE_GREEDY: exact match at temperature 0 (Algorithm 2) */
+} rv_fusion;
+
+typedef struct rv_model rv_model;
+typedef struct rv_cache rv_cache;
+
+/* Status text and the calling thread's last error message. */
+const char* rv_status_str(rv_status s);
+const char* rv_last_error(void);
+
+/* Bytes of device memory a model of this shape needs (weights in the packed
+ * layout the kernels read, norm gains). */
+rv_status rv_model_bytes(const rv_config* cfg, size_t* bytes);
+
+/* Creates a model in the caller's buffer d_buf (>= rv_model_bytes) and fills
+ * it with seeded random-init weights (the paper's trained targets are not
+ * available).  Element (r, c) of logical matrix t (0 embedding,
+ * 1+7l+{q,k,v,o,gate,up,down}, 1+7L LM head) has index i = r*in + c and value
+ *   h = mix(((t << 36) + i) ^ mix(seed)),  mix(x) = splitmix64 finaliser of
+ *       x + 0x9E3779B97F4A7C15 (Steele, Lea, Flood, OOPSLA 2014);
+ *   s = sum of the four 16-bit fields of h - 2*65535;
+ *   w = fp32(s) * fp32(init_std / sqrt(4 (65536^2 - 1) / 12)), then RNE to dtype.
+ * Norm gains are 1.  Asynchronous on stream.  *out is a host handle; free it
+ * with rv_model_free (which does not touch d_buf). */
+rv_status rv_init_weights(const rv_config* cfg, uint64_t seed, void* d_buf, size_t buf_bytes,
+                          void* stream, rv_model** out);
+void rv_model_free(rv_model* m);
+
+/* Bytes of device memory for a cache of `batch` sequences of up to max_len
+ * positions: the KV cache [layer][b][kv_head][pos][head_dim] (dtype), the
+ * token-id history [b][max_len] (int32), the rotary table and the per-call
+ * workspace for blocks of up to max_block rows per sequence and up to
+ * max_drafts draft tokens. */
+rv_status rv_cache_bytes(const rv_model* m, int32_t batch, int32_t max_len, int32_t max_block,
+                         int32_t max_drafts, size_t* bytes);
+
+/* Creates a cache handle over d_buf (>= rv_cache_bytes).  Uploads the rotary
+ * table (synchronously) and zeroes the buffer.  The model must outlive it. */
+rv_status rv_cache_create(rv_model* m, int32_t batch, int32_t max_len, int32_t max_block,
+                          int32_t max_drafts, void* d_buf, size_t buf_bytes, rv_cache** out);
+void rv_cache_free(rv_cache* c);
+
+/* Prefill.  d_prefix_ids is [batch][ld] int32 on the device; sequence b has
+ * h_prefix_len[b] committed tokens (1 <= L_b <= max_len, L_b <= ld).  Stores
+ * ids[0..L_b-1] in the id history and the KV of positions 0..L_b-2 (the
+ * last committed token is left for the first verify, which scores it as
+ * block row 0).  Asynchronous on stream. */
+rv_status rv_prefill_cache(rv_cache* c, const int32_t* d_prefix_ids, int32_t ld,
+                           const int32_t* h_prefix_len, void* stream);
+
+/* One verification pass (Algorithm 1 with Algorithm 2's rule).
+ *   h_prefix_len [batch]  host: committed length L_b of each sequence;
+ *                         requires max(1, P) <= L_b and L_b - 1 + S <= max_len,
+ *                         S = 1 + 2k + n_probe + P <= max_block.
+ *   d_draft_ids [batch][k] device int32, 0 <= k <= max_drafts.
+ *   d_probe_ids [n_probe]  device int32, shared by all sequences (may be
+ *                          NULL when n_probe == 0).
+ *   fusion                 alpha in [0, 1], P >= 0, rule RV_RULE_GREEDY.
+ *   d_accept_len, d_next_id [batch] device int32 outputs: n_b and t_b, or
+ *                          -1 and -1 if any id the block uses is out of range.
+ * Side effects: writes KV at positions L_b-1 .. L_b-2+S (only L_b-1 ..
+ * L_b-1+n_b remain meaningful, the rest is overwritten by later calls, which
+ * prunes the template and second-copy entries, Section 3.1) and appends
+ * x_1..x_n, t to the id history at L_b .. L_b+n.  The caller's next prefix
+ * length is L_b + n_b + 1.  Repeating a call with the same arguments gives
+ * the same outputs.  Asynchronous on stream. */
+rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t k,
+                    const int32_t* d_probe_ids, int32_t n_probe, const rv_fusion* fusion,
+                    int32_t* d_accept_len, int32_t* d_next_id, void* stream);
+
+/* ---- inspection (tests and benchmarks) ---- */
+
+/* Which per-row result of the last rv_verify to copy.  Each is fp32
+ * [batch][k+1][vocab]: raw logits o_i and r_i, fused logits z_i, and their
+ * log-softmax (natural log). */
+enum {
+  RV_OUT_ORIG = 0, RV_OUT_REFL = 1, RV_OUT_FUSED = 2,
+  RV_OUT_LOGP_ORIG = 3, RV_OUT_LOGP_REFL = 4, RV_OUT_LOGP_FUSED = 5
+};
+
+/* Copies one result of the last verify into d_dst (>= batch*(k+1)*vocab*4
+ * bytes).  RV_E_STATE if no verify ran on this cache. Asynchronous. */
+rv_status rv_debug_output(const rv_cache* c, int32_t which, float* d_dst, size_t dst_bytes, void* stream);
+
+/* Copies K and V of one (layer, sequence) for positions [pos0, pos0+npos)
+ * into d_k and d_v, each laid out [kv_head][npos][head_dim] in dtype.
+ * Asynchronous. */
+rv_status rv_debug_export_kv(const rv_cache* c, int32_t layer, int32_t seq, int32_t pos0, int32_t npos,
+                             void* d_k, void* d_v, size_t dst_bytes, void* stream);
+
+/* Copies ids[seq][pos0 .. pos0+n) of the id history into d_dst. Asynchronous. */
+rv_status rv_debug_export_ids(const rv_cache* c, int32_t seq, int32_t pos0, int32_t n, int32_t* d_dst,
+                              void* stream);
+
+/* Stored bits of logical weight elements (synchronous; for bit-equality
+ * checks of the generator).  tensor: 0 embedding, 1+7l+{q,k,v,o,gate,up,down},
+ * 1+7L LM head.  h_idx are flat logical indices r*in + c.  Bits are the bf16
+ * pattern in the low half, or the fp32 pattern. */
+rv_status rv_debug_weight_bits(const rv_model* m, int32_t tensor, const int64_t* h_idx, int32_t n,
+                               uint32_t* h_bits);
+
+/* Intermediate activations of the last prefill or verify pass, for the
+ * rows of that pass (row r = b*S + j for a verify block).  The values are
+ * those of the final layer:
+ *   RV_WS_RESID   fp32 [rows][d_model]     residual stream after the last layer
+ *   RV_WS_ATTN    operand [rows][n_heads*head_dim]  attention output (pre o-proj)
+ *   RV_WS_ACT     operand [rows][ffn_dim]  SwiGLU output (pre down-proj)
+ *   RV_WS_QUERY   operand [rows][n_heads*head_dim]  rotated queries
+ * A matmul operand of a bf16 model is the pair hi = bf16(x), lo = bf16(x - hi)
+ * of its fp32 value x; it is copied as the hi plane followed by the lo plane
+ * ([2][rows][width] bf16).  fp32 models copy [rows][width] fp32.
+ * Asynchronous. */
+enum { RV_WS_RESID = 0, RV_WS_ATTN = 1, RV_WS_ACT = 2, RV_WS_QUERY = 3 };
+rv_status rv_debug_workspace(const rv_cache* c, int32_t which, int32_t rows, void* d_dst, size_t dst_bytes,
+                             void* stream);
+
+/* Fused matrices as the kernels store them. */
+enum { RV_MAT_QKV = 0, RV_MAT_O = 1, RV_MAT_GATEUP = 2, RV_MAT_DOWN = 3, RV_MAT_LM_HEAD = 4 };
+
+/* Y[M][N] = X[M][K] . W^T with the production matrix kernel, for one stored
+ * matrix (layer is ignored for RV_MAT_LM_HEAD).  Columns of Y are in logical
+ * order: QKV = [q rows; k rows; v rows], GATEUP = [gate rows; up rows].
+ * X is the operand form: for bf16 models two planes [2][M][K] bf16 (hi then
+ * lo; X = hi + lo), for fp32 models [M][K] fp32.  Y is fp32 [M][N].
+ * M <= the cache's row capacity.  Asynchronous. */
+rv_status rv_debug_linear(const rv_cache* c, int32_t layer, int32_t matrix, const void* d_x, int32_t M,
+                          float* d_y, size_t y_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* RV_H */

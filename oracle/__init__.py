@@ -21,12 +21,15 @@ Algorithm 1 names are picked out, fused and verified.
 Precision modes:
   "exact"    -- fp64 everywhere (used to pin the decoder against a library
                 implementation);
-  "contract" -- fp64 arithmetic, but values are rounded at the points where
-                the GPU library stores them: fp32 for every matmul result and
-                the residual stream, the storage dtype (bf16 or fp32) for the
-                matmul operands, q/k/v after rotary and the attention output.
-                The only remaining GPU-vs-oracle differences are fp32
-                accumulation order.
+  "contract" -- fp64 arithmetic, but values are rounded where the GPU library
+                stores them: fp32 for every matmul result and the residual
+                stream; K and V to the storage dtype; and every activation
+                that feeds a matmul (norm outputs, rotated q, attention
+                probabilities and output, SwiGLU output) to its operand form.
+                For bf16 models the operand form of an fp32 value x is the
+                pair hi = bf16(x), lo = bf16(x - hi), i.e. about 16
+                significant bits; for fp32 models it is fp32.  The remaining
+                GPU-vs-oracle differences are fp32 accumulation order only.
 """
 from __future__ import annotations
 
@@ -159,6 +162,14 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
     return out
 
 
+def split_bf16(x: np.ndarray) -> np.ndarray:
+    """hi + lo with x32 = fp32(x), hi = bf16(x32), lo = bf16(x32 - hi).
+    x32 - hi is exact in fp32, so the pair is a function of x32 alone."""
+    x32 = round_f32(x)
+    hi = round_bf16(x32)
+    return hi + round_bf16(x32 - hi)
+
+
 class _Rounding:
     def __init__(self, shape, mode: str):
         if mode not in ("exact", "contract"):
@@ -169,11 +180,17 @@ class _Rounding:
     def f32(self, x):
         return x if self.exact else round_f32(x)
 
-    def store(self, x):
-        """Rounding to the storage dtype (matmul operands, q/k/v, attention out)."""
+    def kv(self, x):
+        """K/V cache storage: the model dtype."""
         if self.exact:
             return x
         return round_bf16(x) if self.bf16 else round_f32(x)
+
+    def operand(self, x):
+        """Matmul operand form of an activation: bf16 hi/lo pair or fp32."""
+        if self.exact:
+            return x
+        return split_bf16(x) if self.bf16 else round_f32(x)
 
 
 # ---------------------------------------------------------------- decoder
@@ -251,25 +268,25 @@ def forward(shape, seed: int, tokens: Sequence[int], rows: Sequence[int], mode: 
     h = embedding_rows(shape, seed, tokens)
     ks, vs = [], []
     for l in range(shape.n_layers):
-        a = rnd.store(rms_norm(h, shape.rms_eps))
+        a = rnd.operand(rms_norm(h, shape.rms_eps))
         q = _matmul_wT(shape, seed, l, "q", a, rnd).reshape(n, Hq, hd)
         k = _matmul_wT(shape, seed, l, "k", a, rnd).reshape(n, Hkv, hd)
         v = _matmul_wT(shape, seed, l, "v", a, rnd).reshape(n, Hkv, hd)
-        q = rnd.store(rope(q, cos, sin))
-        k = rnd.store(rope(k, cos, sin))
-        v = rnd.store(v)
+        q = rnd.operand(rope(q, cos, sin))
+        k = rnd.kv(rope(k, cos, sin))
+        v = rnd.kv(v)
         if return_kv:
             ks.append(k)
             vs.append(v)
-        att = rnd.store(causal_attention(q, k, v).reshape(n, Hq * hd))
+        att = rnd.operand(causal_attention(q, k, v).reshape(n, Hq * hd))
         h = rnd.f32(h + _matmul_wT(shape, seed, l, "o", att, rnd))
-        a = rnd.store(rms_norm(h, shape.rms_eps))
+        a = rnd.operand(rms_norm(h, shape.rms_eps))
         g = _matmul_wT(shape, seed, l, "gate", a, rnd)
         u = _matmul_wT(shape, seed, l, "up", a, rnd)
-        act = rnd.store(silu(g) * u)
+        act = rnd.operand(silu(g) * u)
         h = rnd.f32(h + _matmul_wT(shape, seed, l, "down", act, rnd))
     rows = np.asarray(rows, dtype=np.int64)
-    a = rnd.store(rms_norm(h[rows], shape.rms_eps))
+    a = rnd.operand(rms_norm(h[rows], shape.rms_eps))
     logits = _matmul_wT(shape, seed, None, "lm_head", a, rnd)
     if return_kv:
         return logits, np.stack(ks), np.stack(vs)

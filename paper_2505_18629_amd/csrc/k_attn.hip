@@ -1,0 +1,301 @@
+// Block attention against the KV cache.
+//
+// Every query row at position p of sequence b attends the cached keys
+// 0..p of b.  The K/V of the current block were written to the cache by the
+// QKV epilogue of the same layer, so this causal limit is the whole mask:
+// the first draft copy cannot see the probe that follows it (the paper's
+// argument for unidirectional attention, Section 3.1), and the probe and
+// second copy see everything before them.
+//
+// Work split: one workgroup per (key split, query group of 128, segment x kv
+// head).  The G = Hq/Hkv query heads of a kv head share each K/V tile, so a
+// verify block of S rows gives G*S queries per kv head (124 for the 8B shape).
+// Each split writes unnormalised partial results; a second kernel combines
+// splits in a fixed order (deterministic).
+#include "rv_internal.h"
+
+namespace {
+
+constexpr int kKB = 64;  // keys per LDS tile
+
+// ----------------------------------------------------------- bf16, MFMA
+//
+// S^T = K Q^T: A = K tile (16 keys x 32 d), B = Q^T (32 d x 16 queries), so
+// lane l holds the scores of keys 4*(l/16)+i for query l%16.
+// O^T += V^T P^T: A = V^T (16 d x 32 keys) from a transposed LDS copy of V,
+// B = P^T taken directly from the score registers: hardware k slot j of
+// lane group g is key 4g+j (j < 4) of the first 16-key tile and key
+// 16+4g+(j-4) of the second.  P is split into bf16 hi + lo parts (two MFMAs)
+// so the product keeps ~16 significant bits of P.
+template <int HD>
+__global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
+  constexpr int KSTR = HD + 8;     // padded K row (elements)
+  constexpr int VSTR = kKB + 8;    // padded V^T row (elements)
+  constexpr int DC = HD / 32;      // d chunks for QK^T
+  constexpr int DT = HD / 16;      // d tiles for PV
+  __shared__ __attribute__((aligned(16))) uint16_t sK[kKB * KSTR];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[HD * VSTR];
+
+  const int split = blockIdx.x, qg = blockIdx.y, grp = blockIdx.z;
+  const int seg = grp / a.n_kv, kvh = grp % a.n_kv;
+  const int G = a.n_heads / a.n_kv;
+  const int nrows = a.seg_n[seg], row0 = a.seg_row0[seg], pos0 = a.seg_pos0[seg], b = a.seg_b[seg];
+  const int Q = G * nrows;
+  const int q_begin = qg * 128;
+  if (q_begin >= Q) return;
+  const int q_end = min(Q, q_begin + 128);
+  const int kmax = pos0 + (q_end - 1) / G + 1;
+  const int kbeg = split * a.ks, kend = min(kmax, kbeg + a.ks);
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4;
+  const int qd = a.n_heads * HD;
+  const uint16_t* kbase = (const uint16_t*)a.kc + (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
+  const uint16_t* vbase = (const uint16_t*)a.vc + (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
+
+  // Queries of this wave: two 16-query tiles, hi and lo operand planes.
+  uint4 qB[2][2][DC];
+  int qpos[2];
+  bool qvalid[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int q = q_begin + (2 * w + t) * 16 + (lane & 15);
+    qvalid[t] = q < q_end;
+    qpos[t] = qvalid[t] ? pos0 + q / G : -1;
+    const int row = row0 + (qvalid[t] ? q / G : 0), head = kvh * G + (qvalid[t] ? q % G : 0);
+    const size_t off = (size_t)row * qd + head * HD + g * 8;
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl) {
+      const uint16_t* qp = (const uint16_t*)(pl ? a.q2 : a.q) + off;
+#pragma unroll
+      for (int c = 0; c < DC; ++c) qB[pl][t][c] = qvalid[t] ? *(const uint4*)(qp + 32 * c) : uint4{0, 0, 0, 0};
+    }
+  }
+
+  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+  f32x4_t O[2][DT];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int d = 0; d < DT; ++d) O[t][d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int kt0 = kbeg; kt0 < kend; kt0 += kKB) {
+    __syncthreads();
+    // Stage keys [kt0, kt0 + 64) (zeros past kend): K row-major, V transposed.
+    constexpr int CHUNKS = kKB * HD / 8;
+    for (int c = tid; c < CHUNKS; c += 256) {
+      const int kk = c / (HD / 8), d0 = (c % (HD / 8)) * 8;
+      const int key = kt0 + kk;
+      uint4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
+      if (key < kend) {
+        kv = *(const uint4*)(kbase + (size_t)key * HD + d0);
+        vv = *(const uint4*)(vbase + (size_t)key * HD + d0);
+      }
+      *(uint4*)(sK + kk * KSTR + d0) = kv;
+      uint16_t ve[8];
+      memcpy(ve, &vv, 16);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) sV[(d0 + j) * VSTR + kk] = ve[j];
+    }
+    __syncthreads();
+
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      // scores for 64 keys: 4 tiles of 16
+      f32x4_t s[4];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+        s[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < DC; ++c) {
+          const bf16x8_t ka =
+              __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK + (16 * kt + (lane & 15)) * KSTR + 32 * c + g * 8));
+          s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, __builtin_bit_cast(bf16x8_t, qB[0][t][c]), s[kt], 0, 0, 0);
+          s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, __builtin_bit_cast(bf16x8_t, qB[1][t][c]), s[kt], 0, 0, 0);
+        }
+      }
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = kt0 + 16 * kt + 4 * g + i;
+          const bool ok = key < kend && key <= qpos[t];
+          s[kt][i] = ok ? s[kt][i] * a.scale_log2 : -INFINITY;
+          mloc = fmaxf(mloc, s[kt][i]);
+        }
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+      const float m_new = fmaxf(m_run[t], mloc);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;
+      const float rescale = exp2f(m_run[t] - m_use);
+      float psum = 0.f;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          s[kt][i] = exp2f(s[kt][i] - m_use);
+          psum += s[kt][i];
+        }
+      psum += __shfl_xor(psum, 16, 64);
+      psum += __shfl_xor(psum, 32, 64);
+      l_run[t] = l_run[t] * rescale + psum;
+      m_run[t] = m_new;
+#pragma unroll
+      for (int d = 0; d < DT; ++d) O[t][d] *= rescale;
+
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        bf16x8_t phi, plo;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float p = j < 4 ? s[2 * c][j] : s[2 * c + 1][j - 4];
+          const uint16_t hb = f2bf(p);
+          const uint16_t lb = f2bf(p - bf2f(hb));
+          phi[j] = __builtin_bit_cast(__bf16, hb);
+          plo[j] = __builtin_bit_cast(__bf16, lb);
+        }
+#pragma unroll
+        for (int d = 0; d < DT; ++d) {
+          const uint16_t* vrow = sV + (16 * d + (lane & 15)) * VSTR + 32 * c + 4 * g;
+          uint2 v0 = *(const uint2*)vrow;
+          uint2 v1 = *(const uint2*)(vrow + 16);
+          uint4 va = {v0.x, v0.y, v1.x, v1.y};
+          const bf16x8_t vb = __builtin_bit_cast(bf16x8_t, va);
+          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, phi, O[t][d], 0, 0, 0);
+          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, plo, O[t][d], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  // Partials: lane holds O^T[d = 16*dt + 4g + i][query lane%16].
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    if (!qvalid[t]) continue;
+    const int q = q_begin + (2 * w + t) * 16 + (lane & 15);
+    const size_t e = ((size_t)split * (a.nseg * a.n_kv) + grp) * a.qmax + q;
+    float* po = a.part_o + e * HD;
+#pragma unroll
+    for (int d = 0; d < DT; ++d) *(f32x4_t*)(po + 16 * d + 4 * g) = O[t][d];
+    if (g == 0) {
+      a.part_ml[2 * e] = m_run[t];
+      a.part_ml[2 * e + 1] = l_run[t];
+    }
+  }
+}
+
+// ----------------------------------------------------------- fp32, VALU
+// One thread per query; keys read straight from the cache (fp32 models are
+// small).  Same partial format as the MFMA kernel.
+template <int HD>
+__global__ __launch_bounds__(128) void k_attn_f32(AttnArgs a) {
+  const int split = blockIdx.x, grp = blockIdx.z;
+  const int seg = grp / a.n_kv, kvh = grp % a.n_kv;
+  const int G = a.n_heads / a.n_kv;
+  const int nrows = a.seg_n[seg], row0 = a.seg_row0[seg], pos0 = a.seg_pos0[seg], b = a.seg_b[seg];
+  const int q = blockIdx.y * 128 + threadIdx.x;
+  if (q >= G * nrows) return;
+  const int qp = pos0 + q / G;
+  const int kbeg = split * a.ks, kend = min(qp + 1, kbeg + a.ks);
+  const float* qv = (const float*)a.q + (size_t)(row0 + q / G) * (a.n_heads * HD) + (kvh * G + q % G) * HD;
+  const float* kb = (const float*)a.kc + (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
+  const float* vb = (const float*)a.vc + (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
+  float qr[HD], o[HD];
+#pragma unroll
+  for (int d = 0; d < HD; ++d) { qr[d] = qv[d]; o[d] = 0.f; }
+  float m = -INFINITY, l = 0.f;
+  for (int key = kbeg; key < kend; ++key) {
+    float s = 0.f;
+#pragma unroll
+    for (int d = 0; d < HD; ++d) s += qr[d] * kb[(size_t)key * HD + d];
+    s *= a.scale_log2;
+    const float mn = fmaxf(m, s);
+    const float r = exp2f(m - mn), p = exp2f(s - mn);
+    l = l * r + p;
+#pragma unroll
+    for (int d = 0; d < HD; ++d) o[d] = o[d] * r + p * vb[(size_t)key * HD + d];
+    m = mn;
+  }
+  const size_t e = ((size_t)split * (a.nseg * a.n_kv) + grp) * a.qmax + q;
+#pragma unroll
+  for (int d = 0; d < HD; ++d) a.part_o[e * HD + d] = o[d];
+  a.part_ml[2 * e] = m;
+  a.part_ml[2 * e + 1] = l;
+}
+
+// ----------------------------------------------------------- combine
+// One wave per query: merge the splits in index order.
+template <int DT>
+__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a, int hd) {
+  using TR = Tr<DT>;
+  const int lane = threadIdx.x & 63;
+  const int grp = blockIdx.y;
+  const int seg = grp / a.n_kv, kvh = grp % a.n_kv;
+  const int G = a.n_heads / a.n_kv;
+  const int q = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int nrows = a.seg_n[seg];
+  if (q >= G * nrows) return;
+  const int pos_q = a.seg_pos0[seg] + q / G;
+  const size_t stride = (size_t)(a.nseg * a.n_kv) * a.qmax;
+  const size_t e0 = (size_t)grp * a.qmax + q;
+  const int ns = min(a.nsplit, pos_q / a.ks + 1);  // splits that saw keys of this query
+  float M = -INFINITY;
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, a.part_ml[2 * (e0 + s * stride)]);
+  float L = 0.f, acc0 = 0.f, acc1 = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const size_t e = e0 + s * stride;
+    const float ms = a.part_ml[2 * e];
+    const float f = ms == -INFINITY ? 0.f : exp2f(ms - M);
+    L += a.part_ml[2 * e + 1] * f;
+    if (lane < hd) acc0 += a.part_o[e * hd + lane] * f;
+    if (lane + 64 < hd) acc1 += a.part_o[e * hd + lane + 64] * f;
+  }
+  const float inv = 1.0f / L;
+  const int row = a.seg_row0[seg] + q / G, head = kvh * G + q % G;
+  const size_t o = (size_t)row * (a.n_heads * hd) + head * hd;
+  // gather 4 consecutive dims per lane for the operand store
+  const float v0 = acc0 * inv, v1 = acc1 * inv;
+  const int src = (lane & 15) * 4;  // lanes 0..15 store dims 4l..4l+3 of the first 64, 16..31 of the rest
+  f32x4_t x;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float a0 = __shfl(v0, (src + i) & 63, 64);
+    const float a1 = __shfl(v1, (src + i) & 63, 64);
+    x[i] = lane < 16 ? a0 : a1;
+  }
+  if (lane < 16 && 4 * lane < hd) put_operand4<DT>(a.out, a.out2, o + 4 * lane, x);
+  if (lane >= 16 && lane < 32 && 64 + 4 * (lane - 16) < hd) put_operand4<DT>(a.out, a.out2, o + 64 + 4 * (lane - 16), x);
+}
+
+}  // namespace
+
+hipError_t launch_attention(int dtype, const AttnArgs& a, int n_qgroups, hipStream_t st) {
+  const int groups = a.nseg * a.n_kv;
+  if (dtype == RV_BF16) {
+    dim3 grid(a.nsplit, n_qgroups, groups);
+    switch (a.hd) {
+      case 32: k_attn_bf16<32><<<grid, 256, 0, st>>>(a); break;
+      case 64: k_attn_bf16<64><<<grid, 256, 0, st>>>(a); break;
+      case 128: k_attn_bf16<128><<<grid, 256, 0, st>>>(a); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    dim3 grid(a.nsplit, (a.qmax + 127) / 128, groups);
+    switch (a.hd) {
+      case 32: k_attn_f32<32><<<grid, 128, 0, st>>>(a); break;
+      case 64: k_attn_f32<64><<<grid, 128, 0, st>>>(a); break;
+      case 128: k_attn_f32<128><<<grid, 128, 0, st>>>(a); break;
+      default: return hipErrorInvalidValue;
+    }
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_combine(int dtype, const AttnArgs& a, hipStream_t st) {
+  dim3 grid((a.qmax + 3) / 4, a.nseg * a.n_kv);
+  if (dtype == RV_BF16)
+    k_attn_combine<RV_BF16><<<grid, 256, 0, st>>>(a, a.hd);
+  else
+    k_attn_combine<RV_F32><<<grid, 256, 0, st>>>(a, a.hd);
+  return hipGetLastError();
+}

@@ -1,0 +1,128 @@
+// Shared device definitions of the gfx950 verify-pass library.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "rv.h"
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+#define RV_DEV __device__ __forceinline__
+
+// ---------------------------------------------------------------- rounding
+
+// fp32 -> bf16 bits, round to nearest even (finite values; NaN kept quiet).
+RV_DEV uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+RV_DEV float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// Storage type traits: weights, matmul operands and KV are T; a k-step of
+// the matrix kernels consumes one 1 KiB tile of 16 rows x KT elements, in
+// which lane l holds row l % 16 and the VEC consecutive k elements starting
+// at (l / 16) * VEC.
+template <int DT> struct Tr;
+template <> struct Tr<RV_BF16> {
+  typedef uint16_t T;
+  static constexpr int KT = 32, VEC = 8;
+  static RV_DEV T store(float x) { return f2bf(x); }
+  static RV_DEV float load(T x) { return bf2f(x); }
+};
+template <> struct Tr<RV_F32> {
+  typedef float T;
+  static constexpr int KT = 16, VEC = 4;
+  static RV_DEV T store(float x) { return x; }
+  static RV_DEV float load(T x) { return x; }
+};
+
+// One k-step of a 16x16 output tile: acc += A(16 x KT) . B(KT x 16), with A
+// and B given as the 16 bytes each lane holds.  Hardware k slots of lane
+// group g are mapped to logical k = g * VEC + j for both operands, so the
+// reduction covers exactly the tile's KT elements.
+template <int DT> RV_DEV void mma_step(const uint4& a, const uint4& b, f32x4_t& acc);
+template <> RV_DEV void mma_step<RV_BF16>(const uint4& a, const uint4& b, f32x4_t& acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+}
+template <> RV_DEV void mma_step<RV_F32>(const uint4& a, const uint4& b, f32x4_t& acc) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+}
+
+// Operand form of an fp32 activation that feeds a matmul.  bf16 models keep
+// two planes, hi = bf16(x) and lo = bf16(x - hi) (x - hi is exact in fp32),
+// so an operand carries ~16 significant bits and a matmul is two MFMAs;
+// fp32 models keep x in the first plane.
+template <int DT> RV_DEV void put_operand4(void* hi, void* lo, size_t i, const f32x4_t& x);
+template <> RV_DEV void put_operand4<RV_BF16>(void* hi, void* lo, size_t i, const f32x4_t& x) {
+  uint16_t h[4], l[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    h[j] = f2bf(x[j]);
+    l[j] = f2bf(x[j] - bf2f(h[j]));
+  }
+  memcpy((uint16_t*)hi + i, h, 8);
+  memcpy((uint16_t*)lo + i, l, 8);
+}
+template <> RV_DEV void put_operand4<RV_F32>(void* hi, void*, size_t i, const f32x4_t& x) {
+  memcpy((float*)hi + i, &x, 16);
+}
+
+// ---------------------------------------------------------------- packing
+
+// Kinds of stored (fused) matrices.  Physical row order differs from the
+// logical one so that each 16-row tile carries what its epilogue needs:
+//  QKV:    per q/k head, tile j holds dims 8j..8j+7 (rows 0..7) and their
+//          rotate-half partners hd/2+8j.. (rows 8..15); v rows are in order.
+//  GATEUP: tile 2t holds gate rows 16t..16t+15, tile 2t+1 the same up rows.
+enum MatKind { MAT_PLAIN = 0, MAT_QKV = 1, MAT_GATEUP = 2 };
+
+struct MatDesc {
+  int kind;
+  int N, K;                    // physical rows (= logical rows), reduction length
+  int hd, q_rows, k_rows;      // QKV: head_dim, Hq*hd, Hkv*hd
+};
+
+// Logical row of fused-matrix physical row p.
+RV_DEV __host__ inline int mat_logical_row(const MatDesc& m, int p) {
+  if (m.kind == MAT_GATEUP) {
+    int tile = p >> 4, r = p & 15;
+    int half = m.N / 2;
+    return (tile & 1) * half + (tile >> 1) * 16 + r;
+  }
+  if (m.kind == MAT_QKV && p < m.q_rows + m.k_rows) {
+    int head = p / m.hd, within = p % m.hd;
+    int j = within >> 4, r = within & 15;
+    int dim = r < 8 ? 8 * j + r : m.hd / 2 + 8 * j + (r - 8);
+    return head * m.hd + dim;
+  }
+  return p;
+}
+
+// Byte offset of packed element (physical row p, k) for element size es.
+RV_DEV __host__ inline size_t mat_packed_offset(const MatDesc& m, int p, int k, int es) {
+  int vec = 16 / es, kt = 4 * vec;
+  int ksteps = m.K / kt;
+  int tile_k = k / kt, kin = k % kt;
+  int lane = (p & 15) + 16 * (kin / vec);
+  int j = kin % vec;
+  return (((size_t)(p >> 4) * ksteps + tile_k) * 1024) + (size_t)lane * 16 + (size_t)j * es;
+}
+
+// ---------------------------------------------------------------- reductions
+
+RV_DEV float wave_sum(float v) {
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+RV_DEV float wave_max(float v) {
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}

@@ -1,0 +1,143 @@
+// Kernel argument blocks and launchers shared by the host orchestration and
+// the kernel translation units.
+#pragma once
+#include "rv_common.h"
+
+// ---------------------------------------------------------------- init
+hipError_t launch_init_packed(int dtype, void* dst, const MatDesc& md, uint64_t t0, uint64_t t1, uint64_t t2,
+                              int r1, int r2, uint64_t seed_mix, float scale, hipStream_t st);
+hipError_t launch_init_rowmajor(int dtype, void* dst, uint64_t tensor, size_t n, uint64_t seed_mix, float scale,
+                                hipStream_t st);
+hipError_t launch_fill_f32(float* dst, float v, size_t n, hipStream_t st);
+
+// ---------------------------------------------------------------- matrix kernel
+enum EpiKind {
+  EPI_STORE = 0,          // Y[t][p] = acc                        (fp32)
+  EPI_RESID = 1,          // Y[t][p] += acc                       (fp32 residual stream)
+  EPI_SWIGLU = 2,         // act[t][f] = T(silu(gate) * up)       (gate/up tile pairs)
+  EPI_QKV = 3,            // rotary on q/k, q -> qbuf, k/v -> KV cache
+  EPI_STORE_LOGICAL = 4,  // Y[t][logical(p)] = acc               (inspection)
+};
+
+struct GemmArgs {
+  const void* W;      // packed matrix
+  const void* X;      // operand [rows][K]: bf16 hi plane, or fp32; rows padded to the launch's token tiles
+  const void* X2;     // bf16 lo plane (bf16 models)
+  int ldx;
+  int M, N, K;
+  float* Y;           // STORE / RESID / STORE_LOGICAL output, leading dim ldy
+  int ldy;
+  void* act;          // SWIGLU output operand [rows][N/2] (hi plane / fp32)
+  void* act2;         // lo plane
+  int ld_act;
+  // EPI_QKV
+  void* qbuf;         // rotated q operand [rows][Hq*hd] (hi plane / fp32)
+  void* qbuf2;        // lo plane
+  void* kc;           // this layer's K cache [B][Hkv][max_len][hd]
+  void* vc;
+  const int* row_pos;
+  const int* row_seq;
+  const float* rope_cos;  // [max_len][hd/2]
+  const float* rope_sin;
+  int hd, n_heads, n_kv, max_len, q_rows, k_rows;
+  MatDesc md;
+};
+hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- attention
+// Query rows of one pass are grouped in segments (one per sequence and
+// chunk): rows row0 .. row0+n-1 of the row plan at positions pos0 .. pos0+n-1
+// of sequence b.  Query q of (segment, kv head) is row q / G, head kv*G + q % G.
+struct AttnArgs {
+  const void* q;        // rotated q operand [rows][Hq*hd] (hi plane / fp32)
+  const void* q2;       // lo plane
+  const void* kc;       // layer base of the K cache
+  const void* vc;
+  const int* seg_b;
+  const int* seg_row0;
+  const int* seg_n;
+  const int* seg_pos0;
+  int nseg;
+  int n_heads, n_kv, hd, max_len;
+  int ks;               // keys per split (multiple of 64)
+  int nsplit;
+  int qmax;             // query stride per (segment, kv head) in the partial buffers
+  float* part_o;        // [nsplit][nseg*Hkv][qmax][hd]
+  float* part_ml;       // [nsplit][nseg*Hkv][qmax][2]  (running max in log2 units, sum)
+  void* out;            // attention output operand [rows][Hq*hd] (hi plane / fp32)
+  void* out2;           // lo plane
+  float scale_log2;     // log2(e) / sqrt(hd)
+};
+hipError_t launch_attention(int dtype, const AttnArgs& a, int n_qgroups, hipStream_t st);
+hipError_t launch_attn_combine(int dtype, const AttnArgs& a, hipStream_t st);
+
+// ---------------------------------------------------------------- norms and planning
+// RMSNorm of rows of the fp32 residual h into matmul operands (out, out2).  With gather_k >= 0
+// the output row r = b * 2(k+1) + j reads source row b*S + j (j <= k) or
+// b*S + shift + j - (k+1) (the rows the LM head needs).
+hipError_t launch_rmsnorm(int dtype, const float* h, int rows, int d, const float* gain, float eps, void* out,
+                          void* out2, int gather_S, int gather_k, int gather_shift, hipStream_t st);
+
+struct PlanVerify {
+  int B, S, k, n_probe, P, d, V, max_len;
+  const int* ids;        // history [B][max_len]
+  const int* drafts;     // [B][k]
+  const int* probe;      // [n_probe]
+  const void* embed;     // [V][d] T
+  float* h;              // [rows][d]
+  int* row_pos;
+  int* row_seq;
+  int* row_bad;          // [rows]: 1 if the row's id is out of range
+  int* seg_b;
+  int* seg_row0;
+  int* seg_n;
+  int* seg_pos0;
+  int L[RV_MAX_BATCH];
+};
+hipError_t launch_plan_verify(int dtype, const PlanVerify& p, hipStream_t st);
+
+enum { RV_MAX_SEGS = 128 };
+struct PlanPrefill {
+  int nseg, rows, d, V, ld;
+  const int* prefix;     // [B][ld]
+  const void* embed;
+  float* h;
+  int* row_pos;
+  int* row_seq;
+  int* seg_b;
+  int* seg_row0;
+  int* seg_n;
+  int* seg_pos0;
+  int sb[RV_MAX_SEGS], spos0[RV_MAX_SEGS], sn[RV_MAX_SEGS], srow0[RV_MAX_SEGS];
+};
+hipError_t launch_plan_prefill(int dtype, const PlanPrefill& p, hipStream_t st);
+
+struct StoreIds {
+  int B, ld, V, max_len;
+  const int* prefix;
+  int* ids;
+  int* seq_bad;
+  int L[RV_MAX_BATCH];
+};
+hipError_t launch_store_ids(const StoreIds& s, hipStream_t st);
+
+// ---------------------------------------------------------------- LM-head tail
+struct HeadArgs {
+  int B, k, V, S, max_len, nchunk, chunk;
+  float alpha;
+  const float* logits;   // [B][2(k+1)][V]: o rows then r rows per sequence
+  float* z;              // [B][k+1][V]
+  float* part;           // [3 * B*(k+1)][nchunk][4]
+  float* lse;            // [3][B*(k+1)]
+  float* lp;             // [3][B][k+1][V]: log-softmax of o, r, z
+  float* margins;        // [B][k+2]: margins of tested drafts, then top1-top2 gap
+  const int* drafts;     // [B][k]
+  int* ids;              // history [B][max_len]
+  const int* row_bad;    // [B*S]
+  const int* seq_bad;    // [B]
+  int* accept_len;
+  int* next_id;
+  int* argmax;           // [B][k+1]
+  int L[RV_MAX_BATCH];
+};
+hipError_t launch_head(const HeadArgs& a, hipStream_t st);

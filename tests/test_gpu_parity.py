@@ -1,0 +1,230 @@
+"""GPU path vs the CPU oracle on small configurations (through the C ABI).
+
+Bars: accept_len / next_id identical unless the oracle flags a near-tie
+(a decision margin within 1e-3 in fused-logit units); logits max-abs <= 1e-4
+for fp32 models, per-row max|diff| / max|ref| <= 2e-2 for bf16 models;
+log-softmax rows sum to 1.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workload
+
+pytestmark = pytest.mark.gpu
+
+F32_ATOL = 1e-4
+BF16_REL = 2e-2
+
+
+def logits_close(shape, got, ref):
+    got = np.asarray(got, dtype=np.float64)
+    if shape.dtype == "f32":
+        err = np.abs(got - ref).max()
+        assert err <= F32_ATOL, f"max abs logit diff {err}"
+    else:
+        rel = (np.abs(got - ref).max(axis=-1) / np.abs(ref).max(axis=-1)).max()
+        assert rel <= BF16_REL, f"max per-row relative logit diff {rel}"
+
+
+class Case:
+    """Prefill + one verify on the GPU; the oracle recomputes each sequence."""
+
+    def __init__(self, rv, shape, seed, histories, drafts, probe, alpha, P, max_len=None):
+        import torch
+        self.shape, self.seed = shape, seed
+        self.histories = [list(map(int, h)) for h in histories]
+        self.drafts = np.asarray(drafts, dtype=np.int32).reshape(len(histories), -1)
+        self.probe = np.asarray(probe, dtype=np.int32)
+        self.alpha, self.P = alpha, P
+        B = len(histories)
+        k = self.drafts.shape[1]
+        S = 1 + 2 * k + len(self.probe) + P
+        max_len = max_len or (max(len(h) for h in histories) + S + 8)
+        self.v = rv.Verifier(shape, seed, B, max_len, max_block=max(S, 8), max_drafts=max(k, 1))
+        self.lens = self.v.prefill(self.histories)
+        acc, nxt = self.v.verify(self.lens, self.drafts, self.probe, alpha, P)
+        torch.cuda.synchronize()
+        self.accept_len = acc.cpu().numpy().copy()
+        self.next_id = nxt.cpu().numpy().copy()
+        self.out = {w: self.v.output(w).cpu().numpy() for w in range(6)}
+
+    def oracle(self, b):
+        return oracle.verify(self.shape, self.seed, self.histories[b], self.drafts[b], self.probe,
+                             self.alpha, self.P)
+
+    def check(self, rv):
+        for b in range(len(self.histories)):
+            ref = self.oracle(b)
+            logits_close(self.shape, self.out[rv.RV_OUT_ORIG][b], ref["o"])
+            logits_close(self.shape, self.out[rv.RV_OUT_REFL][b], ref["r"])
+            logits_close(self.shape, self.out[rv.RV_OUT_FUSED][b], ref["z"])
+            for w in (rv.RV_OUT_LOGP_ORIG, rv.RV_OUT_LOGP_REFL, rv.RV_OUT_LOGP_FUSED):
+                s = np.exp(self.out[w][b].astype(np.float64)).sum(-1)
+                assert np.abs(s - 1).max() < 1e-4
+            lp_ref = ref["lp_z"]
+            assert np.abs(self.out[rv.RV_OUT_LOGP_FUSED][b] - lp_ref).max() < (
+                1e-4 if self.shape.dtype == "f32" else 0.05 * np.abs(lp_ref).max())
+            if not ref["near_tie"]:
+                assert (int(self.accept_len[b]), int(self.next_id[b])) == (ref["accept_len"], ref["next_id"]), (
+                    b, ref["margins"], ref["gap"])
+        return True
+
+
+def tiny_histories(shape, B, L, key):
+    return [workload.random_ids(shape.vocab, L + 3 * b, key, b) for b in range(B)]
+
+
+@pytest.mark.parametrize("shape", [workload.TINY, workload.TINY_GQA_BF16], ids=lambda s: s.name)
+def test_weights_bit_exact(rv, gpu, shape):
+    import torch
+    v = rv.Verifier(shape, 11, 1, 64)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    names = ["embed"] + [(l, n) for l in range(shape.n_layers) for n in oracle.TENSOR_NAMES] + ["lm_head"]
+    for t, nm in enumerate(names):
+        layer, name = (None, nm) if isinstance(nm, str) else nm
+        rows, cols = oracle.tensor_dims(shape, name)
+        idx = np.unique(np.concatenate([rng.integers(0, rows * cols, 300), [0, rows * cols - 1, cols, cols - 1]]))
+        got = rv.rv_debug_weight_bits(v.model, t, idx)
+        exp = oracle.weight_bits(shape, 11, layer, name, idx.astype(np.uint64))
+        np.testing.assert_array_equal(got, exp, err_msg=f"tensor {t} {nm}")
+    v.close()
+
+
+def draft_case(shape, seed, hist, k, p, key):
+    g = oracle.greedy_continuation(shape, seed, hist, k)
+    return list(workload.corrupt(g, p, shape.vocab, np.random.default_rng(key)))
+
+
+@pytest.mark.parametrize("alpha,P,n_probe,k", [(0.3, 4, 8, 4), (0.0, 4, 8, 4), (1.0, 4, 8, 4), (0.3, 0, 0, 4),
+                                               (0.3, 4, 0, 1), (0.0, 0, 0, 0), (0.3, 2, 5, 6)])
+def test_tiny_f32_matches_oracle(rv, gpu, alpha, P, n_probe, k):
+    shape = workload.TINY
+    hist = list(workload.random_ids(shape.vocab, 128, 0, 0, 2))
+    drafts = draft_case(shape, 0, hist, k, 0.3, 17) if k else []
+    probe = workload.random_ids(shape.vocab, n_probe, 0, 0xBEEF)
+    c = Case(rv, shape, 0, [hist], [drafts], probe, alpha, P)
+    c.check(rv)
+    c.v.close()
+
+
+def test_tiny_f32_batch_ragged(rv, gpu):
+    shape = workload.TINY
+    hists = [workload.random_ids(shape.vocab, L, 1, b) for b, L in enumerate([5, 77, 130, 64])]
+    drafts = [draft_case(shape, 0, h, 4, 0.3, 30 + b) for b, h in enumerate(hists)]
+    probe = workload.random_ids(shape.vocab, 8, 1, 0xBEEF)
+    c = Case(rv, shape, 0, hists, drafts, probe, 0.3, 4)
+    c.check(rv)
+    c.v.close()
+
+
+@pytest.mark.parametrize("alpha,P,n_probe,k", [(0.3, 4, 8, 4), (1.0, 2, 3, 2), (0.0, 0, 0, 0)])
+def test_tiny_bf16_gqa_matches_oracle(rv, gpu, alpha, P, n_probe, k):
+    shape = workload.TINY_GQA_BF16
+    hists = [workload.random_ids(shape.vocab, L, 2, b) for b, L in enumerate([40, 150, 300])]
+    drafts = [draft_case(shape, 1, h, k, 0.3, 40 + b) if k else [] for b, h in enumerate(hists)]
+    probe = workload.random_ids(shape.vocab, n_probe, 2, 0xBEEF)
+    c = Case(rv, shape, 1, hists, drafts, probe, alpha, P)
+    c.check(rv)
+    c.v.close()
+
+
+def test_kv_cache_matches_oracle(rv, gpu):
+    """Prefill + verify write the KV the oracle computes at every position."""
+    import torch
+    shape = workload.TINY_GQA_BF16
+    hist = list(workload.random_ids(shape.vocab, 90, 3, 0))
+    drafts = list(workload.random_ids(shape.vocab, 3, 3, 1))
+    probe = workload.random_ids(shape.vocab, 4, 3, 2)
+    c = Case(rv, shape, 2, [hist], [drafts], probe, 0.3, 4)
+    block, _, _, _ = oracle.reflective_block(hist, drafts, probe, 4)
+    seq = hist[:-1] + block
+    _, ks, vs = oracle.forward(shape, 2, seq, [0], return_kv=True)
+    n = len(seq)
+    for layer in range(shape.n_layers):
+        dk = torch.empty((shape.n_kv_heads, n, shape.head_dim), dtype=torch.bfloat16, device="cuda")
+        dv = torch.empty_like(dk)
+        rv.rv_debug_export_kv(c.v.cache, layer, 0, 0, n, dk, dv)
+        torch.cuda.synchronize()
+        gk = dk.float().cpu().numpy().transpose(1, 0, 2)
+        gv = dv.float().cpu().numpy().transpose(1, 0, 2)
+        for got, ref in ((gk, ks[layer]), (gv, vs[layer])):
+            rel = np.abs(got - ref).max() / np.abs(ref).max()
+            assert rel < 2e-2, (layer, rel)
+            # most elements agree to the last bf16 bit
+            assert np.mean(got == ref) > 0.9
+    c.v.close()
+
+
+def test_history_commit_and_idempotence(rv, gpu):
+    import torch
+    shape = workload.TINY
+    hist = list(workload.random_ids(shape.vocab, 60, 4, 0))
+    drafts = draft_case(shape, 0, hist, 4, 0.0, 4)  # uncorrupted greedy drafts
+    probe = workload.random_ids(shape.vocab, 8, 4, 2)
+    c = Case(rv, shape, 0, [hist], [drafts], probe, 0.0, 4)
+    n, t = int(c.accept_len[0]), int(c.next_id[0])
+    assert n == 4
+    ids = torch.empty(len(hist) + n + 1, dtype=torch.int32, device="cuda")
+    rv.rv_debug_export_ids(c.v.cache, 0, 0, len(hist) + n + 1, ids)
+    torch.cuda.synchronize()
+    assert ids.cpu().tolist() == hist + drafts[:n] + [t]
+    # same call again: same outputs bit for bit
+    z1 = c.out[rv.RV_OUT_FUSED].copy()
+    acc, nxt = c.v.verify(c.lens, c.drafts, c.probe, 0.0, 4)
+    torch.cuda.synchronize()
+    assert (int(acc[0]), int(nxt[0])) == (n, t)
+    np.testing.assert_array_equal(c.v.output(rv.RV_OUT_FUSED).cpu().numpy(), z1)
+    # next step from the committed state continues the greedy sequence
+    g = oracle.greedy_continuation(shape, 0, hist, 6)
+    acc, nxt = c.v.verify([len(hist) + n + 1], np.array([[g[5]]]), [], 0.0, 0)
+    torch.cuda.synchronize()
+    assert int(acc[0]) == 1
+    c.v.close()
+
+
+def test_out_of_range_ids_reported(rv, gpu):
+    import torch
+    shape = workload.TINY
+    v = rv.Verifier(shape, 0, 2, 64, max_block=16, max_drafts=4)
+    lens = v.prefill([list(range(10)), list(range(20, 40))])
+    acc, nxt = v.verify(lens, np.array([[1, 2], [3, shape.vocab + 5]]), [7], 0.3, 2)
+    torch.cuda.synchronize()
+    assert int(acc[1]) == -1 and int(nxt[1]) == -1
+    assert int(acc[0]) >= 0
+    v.close()
+
+
+def test_validation_errors_enqueue_nothing(rv, gpu):
+    import torch
+    shape = workload.TINY
+    v = rv.Verifier(shape, 0, 1, 40, max_block=16, max_drafts=4)
+    lens = v.prefill([list(range(10))])
+    d = torch.zeros((1, 2), dtype=torch.int32, device="cuda")
+    probe = torch.zeros(3, dtype=torch.int32, device="cuda")
+
+    def code(**kw):
+        args = dict(prefix_len=lens, draft_ids=d, k=2, probe_ids=probe, n_probe=3, alpha=0.3, prefix_pos=2,
+                    accept_len=v.accept_len, next_id=v.next_id)
+        args.update(kw)
+        try:
+            rv.rv_verify(v.cache, **args)
+        except rv.RVError as e:
+            return e.name
+        return "RV_OK"
+
+    assert code(alpha=1.5) == "RV_E_ARG"
+    assert code(alpha=float("nan")) == "RV_E_ARG"
+    assert code(k=-1) == "RV_E_ARG"
+    assert code(k=5) == "RV_E_ARG"
+    assert code(prefix_pos=-1) == "RV_E_ARG"
+    assert code(rule=3) == "RV_E_ARG"
+    assert code(prefix_len=[1], prefix_pos=2) == "RV_E_RANGE"
+    assert code(prefix_len=[41]) == "RV_E_RANGE"
+    assert code(prefix_len=[35]) == "RV_E_CAPACITY"
+    assert code(n_probe=12) == "RV_E_CAPACITY"
+    assert code(probe_ids=None) == "RV_E_ARG"
+    assert code() == "RV_OK"
+    torch.cuda.synchronize()
+    v.close()
