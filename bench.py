@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Throughput of the Reflective Verification verify pass on one MI355X.
+
+One step = one rv_verify call: the whole pass (block assembly, all decoder
+layers over the block against the KV cache, LM head on the 2(k+1) rows per
+sequence, fusion, log-softmax, accept and commit).  Inputs and the cache are
+resident in HBM before the timed region; repeated calls are idempotent, so
+the same step is timed K times.
+
+Default workload: the 8B-shaped bf16 model (32 layers, d 4096, 32/8 heads x
+128, FFN 14336, vocab 128256), batch 1, prefix 1024, k = 5 drafts from the
+model's own greedy continuation with random replacement p = 0.3, probe of 16
+ids, prefix-position length 4, alpha = 0.3.  Weights are seeded random-init
+(the paper's trained targets are not available); cost depends only on shapes.
+
+Prints one JSON line.  See --help for options.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_bytes(shape, lens, S, k):
+    """Weights streamed once + KV of the prefix read once + block KV written."""
+    d, hd, F, V, L = shape.d_model, shape.head_dim, shape.ffn_dim, shape.vocab, shape.n_layers
+    qd, kvd = shape.n_heads * hd, shape.n_kv_heads * hd
+    w = 2 if shape.dtype == "bf16" else 4
+    layer_w = (d * (qd + 2 * kvd) + qd * d + 2 * F * d + F * d) * w
+    weights = L * layer_w + V * d * w
+    kv_row = 2 * kvd * w * L
+    kv_read = sum(int(x) - 1 for x in lens) * kv_row
+    kv_write = len(lens) * S * kv_row
+    return weights + kv_read + kv_write
+
+
+def gateup_bytes(shape, M):
+    """Algorithmic bytes of one gate/up launch: the weight stream plus the
+    operand read (hi+lo planes) and the SwiGLU operand written."""
+    d, F = shape.d_model, shape.ffn_dim
+    return 2 * F * d * 2 + M * d * 4 + M * F * 4
+
+
+def source_hash(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_from_profiles(kernel_src):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if
+    it was taken on the current kernel source; else None."""
+    p = os.path.join(ROOT, "profiles", "gateup_8b_b1_counters.json")
+    if not os.path.exists(p):
+        return None
+    try:
+        rec = json.load(open(p))
+    except Exception:
+        return None
+    if rec.get("kernel_source_sha256_16") != source_hash(kernel_src):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def build_state(rv, w, case=0):
+    import torch
+    import workload as wl
+    shape = w.shape
+    lens = wl.prefix_lengths(w, case)
+    prefixes = wl.prefix_ids(w, lens, case)
+    S = w.rows_per_seq
+    max_len = int(max(lens)) + S + w.k + 8
+    v = rv.Verifier(shape, w.weight_seed, w.batch, max_len, max_block=max(64, S), max_drafts=max(16, w.k))
+    v.prefill([list(map(int, p)) for p in prefixes])
+    # the target's own greedy continuation, one single-row verify per token
+    greedy = np.zeros((w.batch, w.k), dtype=np.int32)
+    cur = [int(x) for x in lens]
+    empty = np.zeros((w.batch, 0), dtype=np.int32)
+    for j in range(w.k):
+        _, nxt = v.verify(cur, empty, [], 0.0, 0)
+        greedy[:, j] = nxt.cpu().numpy()
+        cur = [c + 1 for c in cur]
+    ps = wl.replace_probs(w, case)
+    drafts = np.stack([wl.corrupt(greedy[b], ps[b], shape.vocab, wl.draft_rng(w, case, b)) for b in range(w.batch)])
+    probe = wl.probe_ids(w)
+    torch.cuda.synchronize()
+    return v, [int(x) for x in lens], drafts, probe
+
+
+def cpu_baseline(w, lens, drafts, probe, layers=2):
+    """The CPU oracle on a bounded sample of the same step: the from-scratch
+    forward over prefix + block for `layers` of the model's layers plus the LM
+    head on the 2(k+1) rows, fusion and accept, for sequence 0; the layer time
+    is scaled to the full depth."""
+    import oracle
+    import workload as wl
+    shape = w.shape
+    sample = shape.with_layers(layers)
+    prefix = [int(t) for t in wl.prefix_ids(w, lens, 0)[0]]
+    t0 = time.perf_counter()
+    oracle.verify(sample, w.weight_seed, prefix, drafts[0], probe, w.alpha, w.prefix_pos)
+    t_sample = time.perf_counter() - t0
+    # split the sample into per-layer and fixed (LM head, fusion) parts by a
+    # second run with one layer
+    one = shape.with_layers(1)
+    t0 = time.perf_counter()
+    oracle.verify(one, w.weight_seed, prefix, drafts[0], probe, w.alpha, w.prefix_pos)
+    t_one = time.perf_counter() - t0
+    per_layer = max(t_sample - t_one, 1e-9) / (layers - 1)
+    fixed = max(t_one - per_layer, 0.0)
+    t_step = fixed + per_layer * shape.n_layers
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    try:
+        from threadpoolctl import threadpool_info
+        info = threadpool_info()
+        if info:
+            threads = max(i.get("num_threads", 0) for i in info)
+    except Exception:
+        pass
+    return {
+        "value": 1.0 / (t_step * w.batch),  # the oracle verifies one sequence at a time
+        "unit": "verify steps/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"sequence 0 of the workload: from-scratch fp64 forward over its {lens[0]}-token prefix + "
+                   f"{w.rows_per_seq}-row block with {layers} and 1 of {shape.n_layers} layers plus LM head, fusion "
+                   f"and accept; per-layer time scaled to {shape.n_layers} layers (measured {t_sample + t_one:.1f} s)"),
+        "seconds_per_step_est": t_step,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="8b-bf16-b1")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-steps", type=int, default=5)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the verify pass shards by sequence "
+              "across data-parallel replicas; see the design notes). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2505_18629_amd as rv
+    import workload as wl
+
+    w = wl.WORKLOADS[args.workload]
+    shape = w.shape
+    print(f"[bench] workload {w.name}: building model and cache", file=sys.stderr, flush=True)
+    v, lens, drafts, probe = build_state(rv, w)
+    S = w.rows_per_seq
+    d_dr = torch.from_numpy(np.ascontiguousarray(drafts.astype(np.int32))).cuda()
+    d_pr = torch.from_numpy(probe.astype(np.int32)).cuda() if len(probe) else None
+    stream = torch.cuda.current_stream()
+
+    def step():
+        rv.rv_verify(v.cache, lens, d_dr, w.k, d_pr, len(probe), w.alpha, w.prefix_pos, v.accept_len, v.next_id,
+                     stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done ({args.warmup} steps)", file=sys.stderr, flush=True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms = e0.elapsed_time(e1) / args.steps
+    print(f"[bench] timed {args.steps} steps: {ms:.3f} ms/step", file=sys.stderr, flush=True)
+    accept = v.accept_len.cpu().numpy().tolist()
+
+    # per-kernel-class durations from HIP events on the same stream
+    rv.rv_debug_profile(v.cache, True)
+    for _ in range(args.profile_steps):
+        step()
+    torch.cuda.synchronize()
+    per_class = {}
+    for i, name in enumerate(rv.PROF_CLASSES):
+        tot, n = rv.rv_debug_profile_read(v.cache, i)
+        per_class[name] = {"ms_per_launch": tot / n if n else None, "launches_per_step": n // args.profile_steps,
+                           "ms_per_step": tot / args.profile_steps}
+    rv.rv_debug_profile(v.cache, False)
+
+    step_bytes = algorithmic_bytes(shape, lens, S, w.k)
+    steps_per_s = 1000.0 / ms
+    gbs = step_bytes / (ms * 1e-3) / 1e9
+    M = w.batch * S
+    gu_bytes = gateup_bytes(shape, M)
+    gu_ms = per_class["gateup"]["ms_per_launch"]
+    gu_gbs = gu_bytes / (gu_ms * 1e-3) / 1e9 if gu_ms else None
+    kernel_src = os.path.join(ROOT, "paper_2505_18629_amd", "csrc", "k_gemm.hip")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, lens, drafts, probe)
+
+    out = {
+        "metric": "verify steps/s (+ draft tokens verified/s, HBM GB/s)",
+        "value": steps_per_s,
+        "unit": "verify steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": shape.dtype,
+        "data": "synthetic (seeded random-init weights and token ids)",
+        "config": {"workload": w.name, "layers": shape.n_layers, "d_model": shape.d_model,
+                   "heads": f"{shape.n_heads}/{shape.n_kv_heads}x{shape.head_dim}", "ffn": shape.ffn_dim,
+                   "vocab": shape.vocab, "batch": w.batch, "prefix_len": lens if w.batch <= 4 else
+                   [int(min(lens)), int(max(lens))], "k": w.k, "n_probe": w.n_probe, "prefix_pos": w.prefix_pos,
+                   "alpha": w.alpha, "block_rows_per_seq": S, "parallelism": "single GPU"},
+        "draft_tokens_per_s": steps_per_s * w.batch * w.k,
+        "hbm_gbs": gbs,
+        "hbm_frac": gbs / HBM_PEAK_GBS,
+        "algorithmic_bytes_per_step": step_bytes,
+        "wall_s_timed": t_wall,
+        "accept_len": accept,
+        "roofline": {"kernel": "gate/up matmul + SwiGLU", "bound": "hbm", "achieved": gu_gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": (gu_gbs / HBM_PEAK_GBS) if gu_gbs else None,
+                     "algorithmic_bytes_per_launch": gu_bytes, "ms_per_launch": gu_ms,
+                     "traffic": traffic_from_profiles(kernel_src)},
+        "kernel_ms_per_step": {k: round(v_["ms_per_step"], 4) for k, v_ in per_class.items()},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    v.close()
+
+
+if __name__ == "__main__":
+    main()

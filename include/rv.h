@@ -189,6 +189,22 @@ enum { RV_WS_RESID = 0, RV_WS_ATTN = 1, RV_WS_ACT = 2, RV_WS_QUERY = 3 };
 rv_status rv_debug_workspace(const rv_cache* c, int32_t which, int32_t rows, void* d_dst, size_t dst_bytes,
                              void* stream);
 
+/* Kernel classes of the event profiler. */
+enum {
+  RV_PROF_PLAN = 0, RV_PROF_NORM = 1, RV_PROF_QKV = 2, RV_PROF_ATTN = 3, RV_PROF_COMBINE = 4, RV_PROF_O = 5,
+  RV_PROF_GATEUP = 6, RV_PROF_DOWN = 7, RV_PROF_LMHEAD = 8, RV_PROF_TAIL = 9, RV_PROF_NCLASS = 10
+};
+
+/* enable != 0: discard earlier records and, from now on, record a HIP event
+ * pair on the call's stream around every kernel launch of prefill and verify
+ * (the events add a little time between launches, so timing runs keep this
+ * off).  enable == 0 stops recording. */
+rv_status rv_debug_profile(rv_cache* c, int32_t enable);
+
+/* Sum of the recorded durations (ms) and number of launches of one kernel
+ * class.  The caller must have synchronised the stream. */
+rv_status rv_debug_profile_read(const rv_cache* c, int32_t kclass, double* total_ms, int32_t* launches);
+
 /* Fused matrices as the kernels store them. */
 enum { RV_MAT_QKV = 0, RV_MAT_O = 1, RV_MAT_GATEUP = 2, RV_MAT_DOWN = 3, RV_MAT_LM_HEAD = 4 };
 

@@ -33,6 +33,7 @@ RV_MAX_BATCH, RV_MAX_DRAFTS = 256, 32
 RV_OUT_ORIG, RV_OUT_REFL, RV_OUT_FUSED, RV_OUT_LOGP_ORIG, RV_OUT_LOGP_REFL, RV_OUT_LOGP_FUSED = range(6)
 RV_MAT_QKV, RV_MAT_O, RV_MAT_GATEUP, RV_MAT_DOWN, RV_MAT_LM_HEAD = range(5)
 RV_WS_RESID, RV_WS_ATTN, RV_WS_ACT, RV_WS_QUERY = range(4)
+PROF_CLASSES = ["plan", "norm", "qkv", "attn", "combine", "o", "gateup", "down", "lmhead", "tail"]
 STATUS = {0: "RV_OK", -1: "RV_E_ARG", -2: "RV_E_RANGE", -3: "RV_E_CAPACITY", -4: "RV_E_BUFFER",
           -5: "RV_E_HIP", -6: "RV_E_STATE"}
 
@@ -40,7 +41,7 @@ EXPORTED = [
     "rv_status_str", "rv_last_error", "rv_model_bytes", "rv_init_weights", "rv_model_free",
     "rv_cache_bytes", "rv_cache_create", "rv_cache_free", "rv_prefill_cache", "rv_verify",
     "rv_debug_output", "rv_debug_export_kv", "rv_debug_export_ids", "rv_debug_weight_bits",
-    "rv_debug_linear", "rv_debug_workspace",
+    "rv_debug_linear", "rv_debug_workspace", "rv_debug_profile", "rv_debug_profile_read",
 ]
 
 
@@ -81,6 +82,8 @@ _sig = {
     "rv_debug_weight_bits": ([_vp, _i32, _vp, _i32, _vp], ctypes.c_int),
     "rv_debug_linear": ([_vp, _i32, _i32, _vp, _i32, _vp, _sz, _vp], ctypes.c_int),
     "rv_debug_workspace": ([_vp, _i32, _i32, _vp, _sz, _vp], ctypes.c_int),
+    "rv_debug_profile": ([_vp, _i32], ctypes.c_int),
+    "rv_debug_profile_read": ([_vp, _i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i32)], ctypes.c_int),
 }
 for _name, (_args, _res) in _sig.items():
     _f = getattr(_lib, _name)
@@ -208,6 +211,17 @@ def rv_debug_linear(cache: int, layer: int, matrix: int, x, y, stream=None) -> N
 def rv_debug_workspace(cache: int, which: int, rows: int, dst, stream=None) -> None:
     _check(_lib.rv_debug_workspace(cache, which, rows, _dev(dst), dst.numel() * dst.element_size(),
                                    _stream(stream)))
+
+
+def rv_debug_profile(cache: int, enable: bool) -> None:
+    _check(_lib.rv_debug_profile(cache, 1 if enable else 0))
+
+
+def rv_debug_profile_read(cache: int, kclass: int):
+    """(total ms, launches) of one kernel class since profiling was enabled."""
+    ms, n = ctypes.c_double(), _i32()
+    _check(_lib.rv_debug_profile_read(cache, kclass, ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
 
 
 # ------------------------------------------------------------------- buffers

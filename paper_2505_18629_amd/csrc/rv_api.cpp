@@ -99,6 +99,14 @@ struct rv_cache {
   float *logits, *z, *lp, *hpart, *lse, *margins;
   int* argmax;
   int last_k = -1;
+  // event profiler
+  bool prof = false;
+  std::vector<hipEvent_t> prof_ev;   // pairs: start, stop
+  std::vector<int> prof_cls;
+  size_t prof_used = 0;
+  ~rv_cache() {
+    for (hipEvent_t e : prof_ev) (void)hipEventDestroy(e);
+  }
 };
 
 namespace {
@@ -207,6 +215,34 @@ size_t cache_layout(rv_cache* c, void* buf) {
   return align_up(cv.off, kAlign);
 }
 
+// Records a start/stop event pair around one launch when profiling is on.
+struct Prof {
+  rv_cache* c;
+  int cls;
+  hipStream_t st;
+  size_t slot = SIZE_MAX;
+  Prof(rv_cache* c_, int cls_, hipStream_t st_) : c(c_), cls(cls_), st(st_) {
+    if (!c->prof) return;
+    if (c->prof_used == c->prof_cls.size()) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess) return;
+      if (hipEventCreate(&b) != hipSuccess) {
+        (void)hipEventDestroy(a);
+        return;
+      }
+      c->prof_ev.push_back(a);
+      c->prof_ev.push_back(b);
+      c->prof_cls.push_back(-1);
+    }
+    slot = c->prof_used++;
+    c->prof_cls[slot] = cls;
+    (void)hipEventRecord(c->prof_ev[2 * slot], st);
+  }
+  ~Prof() {
+    if (slot != SIZE_MAX) (void)hipEventRecord(c->prof_ev[2 * slot + 1], st);
+  }
+};
+
 // Runs every decoder layer over the current row plan (h filled, segments set).
 // qmax: queries per (segment, kv head); kmax: 1 + largest position in the plan.
 rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, hipStream_t st) {
@@ -247,7 +283,10 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
   for (int l = 0; l < mc.n_layers; ++l) {
     char* kc = c->kc + (size_t)l * c->kv_layer_elems * m->es;
     char* vc = c->vc + (size_t)l * c->kv_layer_elems * m->es;
-    HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n1[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0, st), "rmsnorm");
+    {
+      Prof pf(c, RV_PROF_NORM, st);
+      HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n1[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0, st), "rmsnorm");
+    }
 
     GemmArgs g{};
     g.W = m->w_qkv[l];
@@ -271,12 +310,21 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     g.max_len = c->max_len;
     g.q_rows = m->qkv.q_rows;
     g.k_rows = m->qkv.k_rows;
-    HIP_TRY(launch_gemm(dt, EPI_QKV, g, st), "qkv");
+    {
+      Prof pf(c, RV_PROF_QKV, st);
+      HIP_TRY(launch_gemm(dt, EPI_QKV, g, st), "qkv");
+    }
 
     at.kc = kc;
     at.vc = vc;
-    HIP_TRY(launch_attention(dt, at, qgroups, st), "attention");
-    HIP_TRY(launch_attn_combine(dt, at, st), "attention combine");
+    {
+      Prof pf(c, RV_PROF_ATTN, st);
+      HIP_TRY(launch_attention(dt, at, qgroups, st), "attention");
+    }
+    {
+      Prof pf(c, RV_PROF_COMBINE, st);
+      HIP_TRY(launch_attn_combine(dt, at, st), "attention combine");
+    }
 
     GemmArgs go{};
     go.W = m->w_o[l];
@@ -288,9 +336,15 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     go.K = mc.n_heads * hd;
     go.Y = c->h;
     go.ldy = d;
-    HIP_TRY(launch_gemm(dt, EPI_RESID, go, st), "o-proj");
+    {
+      Prof pf(c, RV_PROF_O, st);
+      HIP_TRY(launch_gemm(dt, EPI_RESID, go, st), "o-proj");
+    }
 
-    HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n2[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0, st), "rmsnorm");
+    {
+      Prof pf(c, RV_PROF_NORM, st);
+      HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n2[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0, st), "rmsnorm");
+    }
     GemmArgs gu{};
     gu.W = m->w_gateup[l];
     gu.X = c->xn;
@@ -302,7 +356,10 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     gu.act = c->act;
     gu.act2 = c->act2;
     gu.ld_act = mc.ffn_dim;
-    HIP_TRY(launch_gemm(dt, EPI_SWIGLU, gu, st), "gate/up");
+    {
+      Prof pf(c, RV_PROF_GATEUP, st);
+      HIP_TRY(launch_gemm(dt, EPI_SWIGLU, gu, st), "gate/up");
+    }
 
     GemmArgs gd{};
     gd.W = m->w_down[l];
@@ -314,7 +371,10 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     gd.K = mc.ffn_dim;
     gd.Y = c->h;
     gd.ldy = d;
-    HIP_TRY(launch_gemm(dt, EPI_RESID, gd, st), "down");
+    {
+      Prof pf(c, RV_PROF_DOWN, st);
+      HIP_TRY(launch_gemm(dt, EPI_RESID, gd, st), "down");
+    }
   }
   return RV_OK;
 }
@@ -540,7 +600,10 @@ rv_status rv_prefill_cache(rv_cache* c, const int32_t* d_prefix_ids, int32_t ld,
     }
     pp.nseg = nseg;
     pp.rows = rows;
-    HIP_TRY(launch_plan_prefill(mc.dtype, pp, st), "prefill plan");
+    {
+      Prof pf(c, RV_PROF_PLAN, st);
+      HIP_TRY(launch_plan_prefill(mc.dtype, pp, st), "prefill plan");
+    }
     rv_status s = run_layers(c, rows, nseg, max_n, kmax, st);
     if (s != RV_OK) return s;
   }
@@ -601,7 +664,10 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   pv.seg_n = c->seg_n;
   pv.seg_pos0 = c->seg_pos0;
   for (int b = 0; b < c->B; ++b) pv.L[b] = h_prefix_len[b];
-  HIP_TRY(launch_plan_verify(dt, pv, st), "verify plan");
+  {
+    Prof pf(c, RV_PROF_PLAN, st);
+    HIP_TRY(launch_plan_verify(dt, pv, st), "verify plan");
+  }
 
   const int M = c->B * (int)S;
   rv_status s = run_layers(c, M, c->B, (int)S, kmax, st);
@@ -610,9 +676,12 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   // LM head on the 2(k+1) rows per sequence that Algorithm 1 reads.
   const int shift = k + n_probe + P;
   const int nout = c->B * 2 * (k + 1);
-  HIP_TRY(launch_rmsnorm(dt, c->h, nout, mc.d_model, m->norm_f, mc.rms_eps, c->lm_x, c->lm_x2, (int)S, k, shift,
-                         st),
-          "final norm");
+  {
+    Prof pf(c, RV_PROF_NORM, st);
+    HIP_TRY(launch_rmsnorm(dt, c->h, nout, mc.d_model, m->norm_f, mc.rms_eps, c->lm_x, c->lm_x2, (int)S, k, shift,
+                           st),
+            "final norm");
+  }
   GemmArgs gl{};
   gl.W = m->lm_head;
   gl.X = c->lm_x;
@@ -623,7 +692,10 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   gl.K = mc.d_model;
   gl.Y = c->logits;
   gl.ldy = mc.vocab;
-  HIP_TRY(launch_gemm(dt, EPI_STORE, gl, st), "lm head");
+  {
+    Prof pf(c, RV_PROF_LMHEAD, st);
+    HIP_TRY(launch_gemm(dt, EPI_STORE, gl, st), "lm head");
+  }
 
   HeadArgs ha{};
   ha.B = c->B;
@@ -648,7 +720,10 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   ha.next_id = d_next_id;
   ha.argmax = c->argmax;
   for (int b = 0; b < c->B; ++b) ha.L[b] = h_prefix_len[b];
-  HIP_TRY(launch_head(ha, st), "accept");
+  {
+    Prof pf(c, RV_PROF_TAIL, st);
+    HIP_TRY(launch_head(ha, st), "accept");
+  }
   c->last_k = k;
   return RV_OK;
 }
@@ -765,6 +840,30 @@ rv_status rv_debug_workspace(const rv_cache* c, int32_t which, int32_t rows, voi
   HIP_TRY(hipMemcpyAsync(d_dst, src, width * rows, hipMemcpyDeviceToDevice, st), "copy");
   if (planes == 2)
     HIP_TRY(hipMemcpyAsync((char*)d_dst + width * rows, src2, width * rows, hipMemcpyDeviceToDevice, st), "copy");
+  return RV_OK;
+}
+
+rv_status rv_debug_profile(rv_cache* c, int32_t enable) {
+  if (!c) return fail(RV_E_ARG, "cache must not be NULL");
+  c->prof = enable != 0;
+  if (c->prof) c->prof_used = 0;
+  return RV_OK;
+}
+
+rv_status rv_debug_profile_read(const rv_cache* c, int32_t kclass, double* total_ms, int32_t* launches) {
+  if (!c || !total_ms || !launches) return fail(RV_E_ARG, "arguments must not be NULL");
+  if (kclass < 0 || kclass >= RV_PROF_NCLASS) return fail(RV_E_ARG, "unknown kernel class %d", kclass);
+  double tot = 0.0;
+  int n = 0;
+  for (size_t i = 0; i < c->prof_used; ++i) {
+    if (c->prof_cls[i] != kclass) continue;
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, c->prof_ev[2 * i], c->prof_ev[2 * i + 1]), "event time");
+    tot += ms;
+    ++n;
+  }
+  *total_ms = tot;
+  *launches = n;
   return RV_OK;
 }
 
