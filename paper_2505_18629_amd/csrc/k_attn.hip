@@ -62,12 +62,13 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
     qvalid[t] = q < q_end;
     qpos[t] = qvalid[t] ? pos0 + q / G : -1;
     const int row = row0 + (qvalid[t] ? q / G : 0), head = kvh * G + (qvalid[t] ? q % G : 0);
-    const size_t off = (size_t)row * qd + head * HD + g * 8;
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl) {
-      const uint16_t* qp = (const uint16_t*)(pl ? a.q2 : a.q) + off;
+      const char* qp = (const char*)(pl ? a.q2 : a.q);
 #pragma unroll
-      for (int c = 0; c < DC; ++c) qB[pl][t][c] = qvalid[t] ? *(const uint4*)(qp + 32 * c) : uint4{0, 0, 0, 0};
+      for (int c = 0; c < DC; ++c)
+        qB[pl][t][c] = qvalid[t] ? *(const uint4*)(qp + operand_offset(row, head * HD + 32 * c + g * 8, qd, 2))
+                                 : uint4{0, 0, 0, 0};
     }
   }
 
@@ -197,12 +198,19 @@ __global__ __launch_bounds__(128) void k_attn_f32(AttnArgs a) {
   if (q >= G * nrows) return;
   const int qp = pos0 + q / G;
   const int kbeg = split * a.ks, kend = min(qp + 1, kbeg + a.ks);
-  const float* qv = (const float*)a.q + (size_t)(row0 + q / G) * (a.n_heads * HD) + (kvh * G + q % G) * HD;
+  const int qrow = row0 + q / G, qcol = (kvh * G + q % G) * HD;
   const float* kb = (const float*)a.kc + (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
   const float* vb = (const float*)a.vc + (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
   float qr[HD], o[HD];
 #pragma unroll
-  for (int d = 0; d < HD; ++d) { qr[d] = qv[d]; o[d] = 0.f; }
+  for (int d = 0; d < HD; d += 4) {
+    const f32x4_t v = *(const f32x4_t*)((const char*)a.q + operand_offset(qrow, qcol + d, a.n_heads * HD, 4));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      qr[d + i] = v[i];
+      o[d + i] = 0.f;
+    }
+  }
   float m = -INFINITY, l = 0.f;
   for (int key = kbeg; key < kend; ++key) {
     float s = 0.f;
@@ -224,10 +232,13 @@ __global__ __launch_bounds__(128) void k_attn_f32(AttnArgs a) {
 }
 
 // ----------------------------------------------------------- combine
-// One wave per query: merge the splits in index order.
+// One wave per query: lane s holds split s's running max and sum (at most 64
+// splits), so the merge weights come from two wave reductions; then each lane
+// accumulates two output dims over the splits in index order.  Loads past
+// the last split read a valid duplicate and get weight 0, so every load is
+// unconditional and batches of 8 are in flight together.
 template <int DT>
 __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a, int hd) {
-  using TR = Tr<DT>;
   const int lane = threadIdx.x & 63;
   const int grp = blockIdx.y;
   const int seg = grp / a.n_kv, kvh = grp % a.n_kv;
@@ -239,20 +250,33 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a, int hd) {
   const size_t stride = (size_t)(a.nseg * a.n_kv) * a.qmax;
   const size_t e0 = (size_t)grp * a.qmax + q;
   const int ns = min(a.nsplit, pos_q / a.ks + 1);  // splits that saw keys of this query
-  float M = -INFINITY;
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, a.part_ml[2 * (e0 + s * stride)]);
-  float L = 0.f, acc0 = 0.f, acc1 = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const size_t e = e0 + s * stride;
-    const float ms = a.part_ml[2 * e];
-    const float f = ms == -INFINITY ? 0.f : exp2f(ms - M);
-    L += a.part_ml[2 * e + 1] * f;
-    if (lane < hd) acc0 += a.part_o[e * hd + lane] * f;
-    if (lane + 64 < hd) acc1 += a.part_o[e * hd + lane + 64] * f;
+  const int sl = min(lane, ns - 1);
+  const float ms = a.part_ml[2 * (e0 + sl * stride)];
+  const float ls = a.part_ml[2 * (e0 + sl * stride) + 1];
+  const float M = wave_max(lane < ns ? ms : -INFINITY);
+  const float f = (lane < ns && ms != -INFINITY) ? exp2f(ms - M) : 0.f;
+  const float L = wave_sum(ls * f);
+  const int d0 = min(lane, hd - 1), d1 = min(lane + 64, hd - 1);
+  float acc0 = 0.f, acc1 = 0.f;
+  for (int s0 = 0; s0 < ns; s0 += 8) {
+    float v0[8], v1[8], fs[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const size_t e = e0 + (size_t)min(s0 + u, ns - 1) * stride;
+      v0[u] = a.part_o[e * hd + d0];
+      v1[u] = a.part_o[e * hd + d1];
+      fs[u] = __shfl(f, (s0 + u) & 63, 64);
+      if (s0 + u >= 64) fs[u] = 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      acc0 += v0[u] * fs[u];
+      acc1 += v1[u] * fs[u];
+    }
   }
   const float inv = 1.0f / L;
   const int row = a.seg_row0[seg] + q / G, head = kvh * G + q % G;
-  const size_t o = (size_t)row * (a.n_heads * hd) + head * hd;
+  const int qd = a.n_heads * hd;
   // gather 4 consecutive dims per lane for the operand store
   const float v0 = acc0 * inv, v1 = acc1 * inv;
   const int src = (lane & 15) * 4;  // lanes 0..15 store dims 4l..4l+3 of the first 64, 16..31 of the rest
@@ -263,8 +287,9 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a, int hd) {
     const float a1 = __shfl(v1, (src + i) & 63, 64);
     x[i] = lane < 16 ? a0 : a1;
   }
-  if (lane < 16 && 4 * lane < hd) put_operand4<DT>(a.out, a.out2, o + 4 * lane, x);
-  if (lane >= 16 && lane < 32 && 64 + 4 * (lane - 16) < hd) put_operand4<DT>(a.out, a.out2, o + 64 + 4 * (lane - 16), x);
+  if (lane < 16 && 4 * lane < hd) put_operand4<DT>(a.out, a.out2, row, head * hd + 4 * lane, qd, x);
+  if (lane >= 16 && lane < 32 && 64 + 4 * (lane - 16) < hd)
+    put_operand4<DT>(a.out, a.out2, row, head * hd + 64 + 4 * (lane - 16), qd, x);
 }
 
 }  // namespace

@@ -1,90 +1,121 @@
 // Weight-streaming matrix kernel: Y[t][p] = sum_k X[t][k] W[p][k] for the
-// few-row activations of a verify block (M = batch * block rows).
+// few-token activations of a verify block (M = batch * block rows) and, with
+// more token groups, for prefill chunks.
 //
 // Layout and schedule
-//  - W is packed in 1 KiB tiles of 16 rows x KT k (see rv_common.h): one
-//    16-byte load per lane reads a whole tile, fully coalesced, already in
-//    MFMA operand order.  Each weight byte is read from HBM once per launch.
-//  - A workgroup owns NT consecutive 16-row tiles and MTT 16-token tiles and
-//    splits K over its 8 waves; the per-wave partial tiles are summed in LDS
-//    in a fixed order (deterministic, no atomics).
-//  - grid.x walks token groups fastest, so launches with more tokens than
-//    one workgroup covers re-read each weight tile from L2, not HBM.
-//  - The epilogue runs on the reduced tile in MFMA output layout: lane l
-//    holds rows 4*(l/16)+i (i = 0..3) of token l%16.
+//  - W is packed in 1 KiB tiles of 16 rows x KT k; activations are stored in
+//    the matching operand tiles (rv_common.h).  One 16-byte load per lane
+//    reads a whole tile, already in MFMA operand order.
+//  - A work item is (token group of MTT tiles, row group of NT tiles, k-group
+//    of K/GK).  Its 4 waves take interleaved k-steps (wave w: steps
+//    kb + w, kb + w + 4, ...) so a workgroup reads one contiguous 4 KiB span
+//    of every row tile per step.
+//  - Each wave keeps the weight and operand tiles of its next DW k-steps in
+//    flight in a register ring.  Loads retire in issue order, so both kinds
+//    share the ring depth.
+//  - The 4 per-wave partial tiles are summed in LDS in a fixed order.  With
+//    GK > 1 the workgroup writes its fp32 partial tile and the consumer (the
+//    next RMSNorm) adds the GK partials in k-group order: deterministic, no
+//    atomics.
+//  - bf16 models multiply every weight tile by both operand planes (hi, lo).
 #include "rv_internal.h"
 
 namespace {
 
-constexpr int kWaves = 8;
+constexpr int kWaves = 4;
+constexpr int kDepth = 4;
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+RV_DEV uint4 load_stream(const uint4* p) {
+  const u32x4_t v = __builtin_nontemporal_load((const u32x4_t*)p);
+  return uint4{v[0], v[1], v[2], v[3]};
+}
 
 RV_DEV float silu(float g) { return g / (1.0f + __expf(-g)); }
 
 template <int DT, int NT, int EPI>
-RV_DEV void epilogue(const GemmArgs& a, int tile0, int tok, int lane, f32x4_t (&v)[NT]) {
+RV_DEV void epilogue(const GemmArgs& a, int tile0, int kg, int tok, int lane, f32x4_t (&v)[NT]) {
   using TR = Tr<DT>;
   using T = typename TR::T;
   const int g = lane >> 4;
   if constexpr (EPI == EPI_STORE || EPI == EPI_RESID) {
     if (tok >= a.M) return;
-    float* y = a.Y + (size_t)tok * a.ldy + tile0 * 16 + 4 * g;
-    f32x4_t r = v[0];
-    if constexpr (EPI == EPI_RESID) r += *(const f32x4_t*)y;
-    *(f32x4_t*)y = r;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      float* y = a.Y + (size_t)tok * a.ldy + (tile0 + nt) * 16 + 4 * g;
+      f32x4_t r = v[nt];
+      if constexpr (EPI == EPI_RESID) r += *(const f32x4_t*)y;
+      *(f32x4_t*)y = r;
+    }
+  } else if constexpr (EPI == EPI_PARTIAL) {
+    if (tok >= a.M) return;
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+      *(f32x4_t*)(a.P + ((size_t)kg * a.M + tok) * a.ldy + (tile0 + nt) * 16 + 4 * g) = v[nt];
   } else if constexpr (EPI == EPI_STORE_LOGICAL) {
     if (tok >= a.M) return;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int p = tile0 * 16 + 4 * g + i;
-      a.Y[(size_t)tok * a.ldy + mat_logical_row(a.md, p)] = v[0][i];
-    }
-  } else if constexpr (EPI == EPI_SWIGLU) {
-    if (tok >= a.M) return;
-    const int f0 = (tile0 >> 1) * 16 + 4 * g;
-    f32x4_t out;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) out[i] = silu(v[0][i]) * v[1][i];
-    put_operand4<DT>(a.act, a.act2, (size_t)tok * a.ld_act + f0, out);
-  } else if constexpr (EPI == EPI_QKV) {
-    // Rotate-half partner of row r (r < 8) is row r + 8, held by lane ^ 32.
-    f32x4_t partner;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) partner[i] = __shfl_xor(v[0][i], 32, 64);
-    if (tok >= a.M) return;
-    const int p0 = tile0 * 16;
-    const int pos = a.row_pos[tok];
-    T out[4];
-    if (p0 < a.q_rows + a.k_rows) {
-      const bool is_q = p0 < a.q_rows;
-      const int rel = is_q ? p0 : p0 - a.q_rows;
-      const int head = rel / a.hd, j = (rel % a.hd) >> 4;
-      const int half = a.hd >> 1;
-      const bool second = lane >= 32;
-      const int r0 = 4 * g - (second ? 8 : 0);      // row within the half, 0..7
-      const float* cs = a.rope_cos + (size_t)pos * half + 8 * j + r0;
-      const float* sn = a.rope_sin + (size_t)pos * half + 8 * j + r0;
-      f32x4_t rot;
+    for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        float c = cs[i], s = sn[i];
-        rot[i] = second ? v[0][i] * c + partner[i] * s : v[0][i] * c - partner[i] * s;
+        const int p = (tile0 + nt) * 16 + 4 * g + i;
+        a.Y[(size_t)tok * a.ldy + mat_logical_row(a.md, p)] = v[nt][i];
       }
-      const int dim = (second ? half : 0) + 8 * j + r0;
-      if (is_q) {
-        put_operand4<DT>(a.qbuf, a.qbuf2, (size_t)tok * (a.n_heads * a.hd) + head * a.hd + dim, rot);
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    // physical tile 2t holds gate rows, 2t+1 the matching up rows
+    if (tok >= a.M) return;
+#pragma unroll
+    for (int nt = 0; nt < NT; nt += 2) {
+      const int f0 = ((tile0 + nt) >> 1) * 16 + 4 * g;
+      f32x4_t out;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) out[i] = silu(v[nt][i]) * v[nt + 1][i];
+      put_operand4<DT>(a.act, a.act2, tok, f0, a.N / 2, out);
+    }
+  } else if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      // Rotate-half partner of row r (r < 8) is row r + 8, held by lane ^ 32.
+      f32x4_t partner;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) partner[i] = __shfl_xor(v[nt][i], 32, 64);
+      if (tok >= a.M) continue;
+      const int p0 = (tile0 + nt) * 16;
+      const int pos = a.row_pos[tok];
+      T out[4];
+      if (p0 < a.q_rows + a.k_rows) {
+        const bool is_q = p0 < a.q_rows;
+        const int rel = is_q ? p0 : p0 - a.q_rows;
+        const int head = rel / a.hd, j = (rel % a.hd) >> 4;
+        const int half = a.hd >> 1;
+        const bool second = lane >= 32;
+        const int r0 = 4 * g - (second ? 8 : 0);  // row within the half, 0..7
+        const float* cs = a.rope_cos + (size_t)pos * half + 8 * j + r0;
+        const float* sn = a.rope_sin + (size_t)pos * half + 8 * j + r0;
+        f32x4_t rot;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float c = cs[i], s = sn[i];
+          rot[i] = second ? v[nt][i] * c + partner[i] * s : v[nt][i] * c - partner[i] * s;
+        }
+        const int dim = (second ? half : 0) + 8 * j + r0;
+        if (is_q) {
+          put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + dim, a.n_heads * a.hd, rot);
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) out[i] = TR::store(rot[i]);
+          const int b = a.row_seq[tok];
+          memcpy((T*)a.kc + ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim, out, sizeof(out));
+        }
       } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) out[i] = TR::store(rot[i]);
+        const int rel = p0 - a.q_rows - a.k_rows + 4 * g;
+        const int head = rel / a.hd, dim = rel % a.hd;
         const int b = a.row_seq[tok];
-        memcpy((T*)a.kc + ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim, out, sizeof(out));
-      }
-    } else {
-      const int rel = p0 - a.q_rows - a.k_rows + 4 * g;
-      const int head = rel / a.hd, dim = rel % a.hd;
-      const int b = a.row_seq[tok];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) out[i] = TR::store(v[0][i]);
-      memcpy((T*)a.vc + ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim, out, sizeof(out));
+        for (int i = 0; i < 4; ++i) out[i] = TR::store(v[nt][i]);
+        memcpy((T*)a.vc + ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim, out, sizeof(out));
+      }
     }
   }
 }
@@ -92,24 +123,26 @@ RV_DEV void epilogue(const GemmArgs& a, int tile0, int tok, int lane, f32x4_t (&
 template <int DT, int NT, int MTT, int EPI>
 __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
   using TR = Tr<DT>;
-  using T = typename TR::T;
-  constexpr int KT = TR::KT, VEC = TR::VEC;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int ksteps = a.K / KT;
-  const int s0 = (w * ksteps) / kWaves, s1 = ((w + 1) * ksteps) / kWaves;
-  const int tok0 = blockIdx.x * (MTT * 16);
-  const int tile0 = blockIdx.y * NT;
-
-  // bf16 models multiply each weight tile by both operand planes (hi, lo).
+  constexpr int KT = TR::KT;
   constexpr int PL = DT == RV_BF16 ? 2 : 1;
-  const uint4* wp = (const uint4*)a.W + (size_t)tile0 * ksteps * 64 + lane;
-  const uint4* xp[PL][MTT];
+  // weights are read exactly once when a single token group covers M
+  constexpr bool kStream = MTT <= 2;
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int ksteps = a.K / KT;
+  const int item = blockIdx.x;
+  const int tg = item % a.n_tg, rest = item / a.n_tg;
+  const int kg = rest % a.gk, rg = rest / a.gk;
+  const int kb = kg * (ksteps / a.gk);
+  const int spr = ksteps / (a.gk * kWaves);  // k-steps per wave
+  const int tile0 = rg * NT;
+  const int tok0 = tg * MTT * 16;
+
+  const uint4* wp = (const uint4*)a.W + (size_t)tile0 * ksteps * 64 + (size_t)(kb + w) * 64 + lane;
+  const uint4* xp[PL];
 #pragma unroll
   for (int pl = 0; pl < PL; ++pl)
-#pragma unroll
-    for (int mt = 0; mt < MTT; ++mt)
-      xp[pl][mt] = (const uint4*)((const T*)(pl ? a.X2 : a.X) + (size_t)(tok0 + mt * 16 + (lane & 15)) * a.ldx +
-                                  (lane >> 4) * VEC);
+    xp[pl] = (const uint4*)(pl ? a.X2 : a.X) + (size_t)(tok0 >> 4) * ksteps * 64 + (size_t)(kb + w) * 64 + lane;
 
   f32x4_t acc[NT][MTT];
 #pragma unroll
@@ -117,21 +150,50 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MTT; ++mt) acc[nt][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-#pragma unroll 4
-  for (int s = s0; s < s1; ++s) {
-    uint4 av[NT], bv[PL][MTT];
+  uint4 wq[kDepth][NT], xq[kDepth][PL][MTT];
+  // the j-th k-step of this wave is kb + w + 4j
+  auto load = [&](int slot, int j) {
+    const size_t o = (size_t)j * (kWaves * 64);
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) av[nt] = wp[((size_t)nt * ksteps + s) * 64];
+    for (int nt = 0; nt < NT; ++nt) {
+      const uint4* p = wp + (size_t)nt * ksteps * 64 + o;
+      wq[slot][nt] = kStream ? load_stream(p) : *p;
+    }
 #pragma unroll
     for (int pl = 0; pl < PL; ++pl)
 #pragma unroll
-      for (int mt = 0; mt < MTT; ++mt) bv[pl][mt] = xp[pl][mt][(size_t)s * (KT / VEC)];
+      for (int mt = 0; mt < MTT; ++mt) xq[slot][pl][mt] = xp[pl][(size_t)mt * ksteps * 64 + o];
+  };
+  auto compute = [&](int slot) {
 #pragma unroll
     for (int pl = 0; pl < PL; ++pl)
 #pragma unroll
       for (int nt = 0; nt < NT; ++nt)
 #pragma unroll
-        for (int mt = 0; mt < MTT; ++mt) mma_step<DT>(av[nt], bv[pl][mt], acc[nt][mt]);
+        for (int mt = 0; mt < MTT; ++mt) mma_step<DT>(wq[slot][nt], xq[slot][pl][mt], acc[nt][mt]);
+  };
+  // Full groups of kDepth steps run branch-free; the last full group only
+  // computes; a remainder (spr not a multiple of kDepth) runs unpipelined.
+  const int nfull = spr / kDepth;
+  int j = 0;
+  if (nfull > 0) {
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) load(d, d);
+    for (int gi = 1; gi < nfull; ++gi) {
+#pragma unroll
+      for (int d = 0; d < kDepth; ++d) {
+        compute(d);
+        load(d, j + kDepth + d);
+      }
+      j += kDepth;
+    }
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) compute(d);
+    j += kDepth;
+  }
+  for (; j < spr; ++j) {
+    load(0, j);
+    compute(0);
   }
 
   __shared__ f32x4_t red[kWaves][NT][MTT][64];
@@ -140,8 +202,7 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
 #pragma unroll
     for (int mt = 0; mt < MTT; ++mt) red[w][nt][mt][lane] = acc[nt][mt];
   __syncthreads();
-  if (w < MTT) {
-    const int mt = w;
+  for (int mt = w; mt < MTT; mt += kWaves) {
     f32x4_t v[NT];
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
@@ -149,40 +210,50 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
 #pragma unroll
       for (int ww = 1; ww < kWaves; ++ww) v[nt] += red[ww][nt][mt][lane];
     }
-    epilogue<DT, NT, EPI>(a, tile0, tok0 + mt * 16 + (lane & 15), lane, v);
+    epilogue<DT, NT, EPI>(a, tile0, kg, tok0 + mt * 16 + (lane & 15), lane, v);
   }
 }
 
 template <int DT, int NT, int EPI>
-hipError_t launch_mtt(const GemmArgs& a, hipStream_t st) {
-  const int rows_per_wg = 16 * NT;
-  dim3 block(kWaves * 64);
-  if (a.M <= 16) {
-    k_gemm<DT, NT, 1, EPI><<<dim3(1, a.N / rows_per_wg), block, 0, st>>>(a);
-  } else if (a.M <= 32) {
-    k_gemm<DT, NT, 2, EPI><<<dim3(1, a.N / rows_per_wg), block, 0, st>>>(a);
-  } else {
-    k_gemm<DT, NT, 4, EPI><<<dim3((a.M + 63) / 64, a.N / rows_per_wg), block, 0, st>>>(a);
+hipError_t launch_nt(const GemmArgs& a, int mtt, hipStream_t st) {
+  const unsigned items = (unsigned)(a.n_tg * a.gk * (a.N / (16 * NT)));
+  const dim3 block(kWaves * 64);
+  switch (mtt) {
+    case 1: k_gemm<DT, NT, 1, EPI><<<items, block, 0, st>>>(a); break;
+    case 2: k_gemm<DT, NT, 2, EPI><<<items, block, 0, st>>>(a); break;
+    case 4: k_gemm<DT, NT, 4, EPI><<<items, block, 0, st>>>(a); break;
+    default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
+template <int DT, int EPI>
+hipError_t launch_epi(const GemmArgs& a, int nt, int mtt, hipStream_t st) {
+  switch (nt) {
+    case 1:
+      if constexpr (EPI != EPI_SWIGLU) return launch_nt<DT, 1, EPI>(a, mtt, st);
+      break;
+    case 2: return launch_nt<DT, 2, EPI>(a, mtt, st);
+    case 4: return launch_nt<DT, 4, EPI>(a, mtt, st);
+  }
+  return hipErrorInvalidValue;
+}
+
 template <int DT>
-hipError_t launch_dt(int epi, const GemmArgs& a, hipStream_t st) {
+hipError_t launch_dt(int epi, const GemmArgs& a, int nt, int mtt, hipStream_t st) {
   switch (epi) {
-    case EPI_STORE: return launch_mtt<DT, 1, EPI_STORE>(a, st);
-    case EPI_RESID: return launch_mtt<DT, 1, EPI_RESID>(a, st);
-    case EPI_SWIGLU: return launch_mtt<DT, 2, EPI_SWIGLU>(a, st);
-    case EPI_QKV: return launch_mtt<DT, 1, EPI_QKV>(a, st);
-    case EPI_STORE_LOGICAL: return launch_mtt<DT, 1, EPI_STORE_LOGICAL>(a, st);
+    case EPI_STORE: return launch_epi<DT, EPI_STORE>(a, nt, mtt, st);
+    case EPI_RESID: return launch_epi<DT, EPI_RESID>(a, nt, mtt, st);
+    case EPI_PARTIAL: return launch_epi<DT, EPI_PARTIAL>(a, nt, mtt, st);
+    case EPI_SWIGLU: return launch_epi<DT, EPI_SWIGLU>(a, nt, mtt, st);
+    case EPI_QKV: return launch_epi<DT, EPI_QKV>(a, nt, mtt, st);
+    case EPI_STORE_LOGICAL: return launch_epi<DT, EPI_STORE_LOGICAL>(a, nt, mtt, st);
   }
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-// Operand rows read: round_up(M, 16) for M <= 32, else round_up(M, 64); the
-// caller's X buffer must hold that many rows.
-hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, hipStream_t st) {
-  return dtype == RV_BF16 ? launch_dt<RV_BF16>(epi, a, st) : launch_dt<RV_F32>(epi, a, st);
+hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, int nt, int mtt, hipStream_t st) {
+  return dtype == RV_BF16 ? launch_dt<RV_BF16>(epi, a, nt, mtt, st) : launch_dt<RV_F32>(epi, a, nt, mtt, st);
 }

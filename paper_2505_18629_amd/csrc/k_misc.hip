@@ -5,21 +5,34 @@ namespace {
 
 // ----------------------------------------------------------- RMSNorm
 // y = h * rsqrt(mean(h^2) + eps) * g, stored as a matmul operand; one
-// 256-thread workgroup per row.
+// 256-thread workgroup per row.  Pending k-group partials of the previous
+// matmul (P, gk) are first added to h in k-group order and h is written back.
 template <int DT>
-__global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h, int d, const float* __restrict__ gain,
+__global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ h, int d, const float* __restrict__ gain,
                                                  float eps, void* __restrict__ out, void* __restrict__ out2, int gS,
-                                                 int gk, int gshift) {
+                                                 int gk, int gshift, const float* __restrict__ P, int pk, int rows) {
   const int r = blockIdx.x;
   int src = r;
   if (gk >= 0) {
     const int per = 2 * (gk + 1), b = r / per, j = r % per;
     src = b * gS + (j <= gk ? j : gshift + j - (gk + 1));
   }
-  const float* x = h + (size_t)src * d;
+  float* x = h + (size_t)src * d;
   float ss = 0.f;
   for (int i = threadIdx.x * 4; i < d; i += 256 * 4) {
-    const f32x4_t v = *(const f32x4_t*)(x + i);
+    f32x4_t v = *(const f32x4_t*)(x + i);
+    if (P) {
+      // batches of 4 independent loads; past the last k-group the load
+      // repeats a valid partial and is weighted 0
+      for (int g0 = 0; g0 < pk; g0 += 4) {
+        f32x4_t pv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) pv[u] = *(const f32x4_t*)(P + ((size_t)min(g0 + u, pk - 1) * rows + src) * d + i);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v += g0 + u < pk ? pv[u] : f32x4_t{0.f, 0.f, 0.f, 0.f};
+      }
+      *(f32x4_t*)(x + i) = v;
+    }
     ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
   }
   ss = wave_sum(ss);
@@ -34,8 +47,19 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const float* __restrict__ h, in
     f32x4_t o;
 #pragma unroll
     for (int j = 0; j < 4; ++j) o[j] = v[j] * rs * gg[j];
-    put_operand4<DT>(out, out2, (size_t)r * d + i, o);
+    put_operand4<DT>(out, out2, r, i, d, o);
   }
+}
+
+// Row-major [rows][K] <-> operand tiles, one element per thread.
+template <typename T>
+__global__ void k_retile(const T* __restrict__ src, T* __restrict__ dst, int rows, int K, bool to_tiles) {
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (size_t)rows * K) return;
+  const int t = (int)(i / K), k = (int)(i % K);
+  const size_t o = operand_offset(t, k, K, sizeof(T)) / sizeof(T);
+  if (to_tiles) dst[o] = src[i];
+  else dst[i] = src[o];
 }
 
 // ----------------------------------------------------------- embedding gather
@@ -117,13 +141,24 @@ __global__ __launch_bounds__(256) void k_store_ids(StoreIds s) {
 
 }  // namespace
 
-hipError_t launch_rmsnorm(int dtype, const float* h, int rows, int d, const float* gain, float eps, void* out,
-                          void* out2, int gS, int gk, int gshift, hipStream_t st) {
+hipError_t launch_rmsnorm(int dtype, float* h, int rows, int d, const float* gain, float eps, void* out,
+                          void* out2, int gS, int gk, int gshift, const float* P, int pk, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
+  // partial rows are indexed by source row; the gathering form never reads partials
   if (dtype == RV_BF16)
-    k_rmsnorm<RV_BF16><<<rows, 256, 0, st>>>(h, d, gain, eps, out, out2, gS, gk, gshift);
+    k_rmsnorm<RV_BF16><<<rows, 256, 0, st>>>(h, d, gain, eps, out, out2, gS, gk, gshift, P, pk, rows);
   else
-    k_rmsnorm<RV_F32><<<rows, 256, 0, st>>>(h, d, gain, eps, out, out2, gS, gk, gshift);
+    k_rmsnorm<RV_F32><<<rows, 256, 0, st>>>(h, d, gain, eps, out, out2, gS, gk, gshift, P, pk, rows);
+  return hipGetLastError();
+}
+
+hipError_t launch_retile(int dtype, const void* src, void* dst, int rows, int K, bool to_tiles, hipStream_t st) {
+  const size_t n = (size_t)rows * K;
+  const dim3 grid((unsigned)((n + 255) / 256));
+  if (dtype == RV_BF16)
+    k_retile<uint16_t><<<grid, 256, 0, st>>>((const uint16_t*)src, (uint16_t*)dst, rows, K, to_tiles);
+  else
+    k_retile<float><<<grid, 256, 0, st>>>((const float*)src, (float*)dst, rows, K, to_tiles);
   return hipGetLastError();
 }
 

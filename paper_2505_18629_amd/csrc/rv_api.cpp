@@ -37,6 +37,8 @@ constexpr size_t kAlign = 256;
 constexpr int kPrefillRows = 2048;   // rows per prefill chunk
 constexpr int kSplitsPerQuery = 8;   // partial-buffer depth per query row
 constexpr int kVocabChunk = 8192;    // vocabulary chunk of the LM-head tail
+constexpr int kMaxSplitK = 16;       // k-groups of a split matmul
+constexpr int kSplitRows = 64;       // matmuls with at most this many rows may split K
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 int round_up(int x, int a) { return (x + a - 1) / a * a; }
@@ -96,6 +98,7 @@ struct rv_cache {
   void *xn, *xn2, *qbuf, *qbuf2, *att, *att2, *act, *act2, *lm_x, *lm_x2;
   size_t part_entries;
   float *part_o, *part_ml;
+  float* gpart;  // k-group partials of a split matmul [kMaxSplitK][kSplitRows][d_model]
   float *logits, *z, *lp, *hpart, *lse, *margins;
   int* argmax;
   int last_k = -1;
@@ -117,7 +120,8 @@ rv_status check_config(const rv_config* c) {
   if (c->n_layers <= 0 || c->d_model <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 || c->ffn_dim <= 0 ||
       c->vocab <= 0)
     return fail(RV_E_ARG, "shape fields must be positive");
-  if (c->d_model % 32 || c->ffn_dim % 32) return fail(RV_E_ARG, "d_model and ffn_dim must be multiples of 32");
+  if (c->d_model % 128 || c->ffn_dim % 128 || (c->n_heads * c->head_dim) % 128)
+    return fail(RV_E_ARG, "d_model, ffn_dim and n_heads*head_dim must be multiples of 128");
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
     return fail(RV_E_ARG, "head_dim must be 32, 64 or 128");
   if (c->n_heads % c->n_kv_heads) return fail(RV_E_ARG, "n_heads must be a multiple of n_kv_heads");
@@ -205,6 +209,7 @@ size_t cache_layout(rv_cache* c, void* buf) {
   c->lm_x2 = cv.take<void*>((size_t)c->out_rows_cap * d * e2);
   c->part_o = cv.take<float*>(c->part_entries * hd * 4);
   c->part_ml = cv.take<float*>(c->part_entries * 2 * 4);
+  c->gpart = cv.take<float*>((size_t)kMaxSplitK * kSplitRows * d * 4);
   c->logits = cv.take<float*>((size_t)c->out_rows_cap * mc.vocab * 4);
   c->z = cv.take<float*>((size_t)c->r1_cap * mc.vocab * 4);
   c->lp = cv.take<float*>((size_t)3 * c->r1_cap * mc.vocab * 4);
@@ -243,6 +248,49 @@ struct Prof {
   }
 };
 
+// Launch shape of one matmul: row tiles per workgroup (nt), token tiles
+// (mtt), token groups and k-groups.  Aims for >= 384 workgroups (1.5 per CU)
+// with as many rows per workgroup as possible, since every workgroup reads
+// its k-range of all operand tiles; K is split across workgroups only for
+// residual-stream outputs of few-row passes (the next RMSNorm adds the
+// partials).
+struct GemmPlan {
+  int nt, mtt, n_tg, gk;
+};
+
+GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K, bool allow_split) {
+  constexpr int kTarget = 384;
+  const int ksteps = K / (dtype == RV_BF16 ? 32 : 16);
+  GemmPlan p{};
+  p.mtt = M <= 16 ? 1 : M <= 32 ? 2 : 4;
+  p.n_tg = (M + 16 * p.mtt - 1) / (16 * p.mtt);
+  p.gk = 1;
+  const int nt_min = epi == EPI_SWIGLU ? 2 : 1;
+  if (allow_split && M <= kSplitRows && N % 64 == 0) {
+    p.nt = 4;
+    const int cand[] = {1, 2, 4, 7, 8, 14, 16};
+    for (int gk : cand) {
+      if (ksteps % (4 * gk)) continue;
+      p.gk = gk;
+      if ((long long)(N / 64) * gk * p.n_tg >= kTarget) break;
+    }
+    return p;
+  }
+  p.nt = 4;
+  while (p.nt > nt_min && (N % (16 * p.nt) || (long long)(N / (16 * p.nt)) * p.n_tg < kTarget)) p.nt /= 2;
+  while (N % (16 * p.nt)) p.nt /= 2;
+  return p;
+}
+
+hipError_t run_gemm(int dtype, int epi, GemmArgs g, bool allow_split, hipStream_t st, int* gk_out = nullptr) {
+  const GemmPlan p = plan_gemm(dtype, epi, g.M, g.N, g.K, allow_split);
+  g.n_tg = p.n_tg;
+  g.gk = p.gk;
+  if (gk_out) *gk_out = p.gk;
+  const int e = (epi == EPI_RESID && p.gk > 1) ? EPI_PARTIAL : epi;
+  return launch_gemm(dtype, e, g, p.nt, p.mtt, st);
+}
+
 // Runs every decoder layer over the current row plan (h filled, segments set).
 // qmax: queries per (segment, kv head); kmax: 1 + largest position in the plan.
 rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, hipStream_t st) {
@@ -254,9 +302,10 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
   const int groups = nseg * mc.n_kv_heads;
   const int qgroups = (qmax + 127) / 128;
   // key split: aim for >= 512 workgroups, bounded by the partial buffer
-  int want = std::max(1, (512 + groups * qgroups - 1) / (groups * qgroups));
+  // (the combine kernel merges at most 64 splits per query)
+  int want = std::min(64, std::max(1, (512 + groups * qgroups - 1) / (groups * qgroups)));
   int ks = round_up((kmax + want - 1) / want, 64);
-  while ((size_t)((kmax + ks - 1) / ks) * groups * qmax > c->part_entries) ks += 64;
+  while ((size_t)((kmax + ks - 1) / ks) * groups * qmax > c->part_entries || (kmax + ks - 1) / ks > 64) ks += 64;
   const int nsplit = (kmax + ks - 1) / ks;
 
   AttnArgs at{};
@@ -280,19 +329,21 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
   at.out2 = c->att2;
   at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)hd));
 
+  int pending = 0;  // k-groups of the last residual matmul still in c->gpart
   for (int l = 0; l < mc.n_layers; ++l) {
     char* kc = c->kc + (size_t)l * c->kv_layer_elems * m->es;
     char* vc = c->vc + (size_t)l * c->kv_layer_elems * m->es;
     {
       Prof pf(c, RV_PROF_NORM, st);
-      HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n1[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0, st), "rmsnorm");
+      HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n1[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0,
+                             pending > 1 ? c->gpart : nullptr, pending, st),
+              "rmsnorm");
     }
 
     GemmArgs g{};
     g.W = m->w_qkv[l];
     g.X = c->xn;
     g.X2 = c->xn2;
-    g.ldx = d;
     g.M = M;
     g.N = m->qkv.N;
     g.K = d;
@@ -312,7 +363,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     g.k_rows = m->qkv.k_rows;
     {
       Prof pf(c, RV_PROF_QKV, st);
-      HIP_TRY(launch_gemm(dt, EPI_QKV, g, st), "qkv");
+      HIP_TRY(run_gemm(dt, EPI_QKV, g, false, st), "qkv");
     }
 
     at.kc = kc;
@@ -330,26 +381,27 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     go.W = m->w_o[l];
     go.X = c->att;
     go.X2 = c->att2;
-    go.ldx = mc.n_heads * hd;
     go.M = M;
     go.N = d;
     go.K = mc.n_heads * hd;
     go.Y = c->h;
     go.ldy = d;
+    go.P = c->gpart;
     {
       Prof pf(c, RV_PROF_O, st);
-      HIP_TRY(launch_gemm(dt, EPI_RESID, go, st), "o-proj");
+      HIP_TRY(run_gemm(dt, EPI_RESID, go, true, st, &pending), "o-proj");
     }
 
     {
       Prof pf(c, RV_PROF_NORM, st);
-      HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n2[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0, st), "rmsnorm");
+      HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n2[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0,
+                             pending > 1 ? c->gpart : nullptr, pending, st),
+              "rmsnorm");
     }
     GemmArgs gu{};
     gu.W = m->w_gateup[l];
     gu.X = c->xn;
     gu.X2 = c->xn2;
-    gu.ldx = d;
     gu.M = M;
     gu.N = m->gateup.N;
     gu.K = d;
@@ -358,22 +410,23 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     gu.ld_act = mc.ffn_dim;
     {
       Prof pf(c, RV_PROF_GATEUP, st);
-      HIP_TRY(launch_gemm(dt, EPI_SWIGLU, gu, st), "gate/up");
+      HIP_TRY(run_gemm(dt, EPI_SWIGLU, gu, false, st), "gate/up");
     }
 
     GemmArgs gd{};
     gd.W = m->w_down[l];
     gd.X = c->act;
     gd.X2 = c->act2;
-    gd.ldx = mc.ffn_dim;
     gd.M = M;
     gd.N = d;
     gd.K = mc.ffn_dim;
     gd.Y = c->h;
     gd.ldy = d;
+    gd.P = c->gpart;
     {
+      // the last layer writes h directly: the LM-head norm gathers rows
       Prof pf(c, RV_PROF_DOWN, st);
-      HIP_TRY(launch_gemm(dt, EPI_RESID, gd, st), "down");
+      HIP_TRY(run_gemm(dt, EPI_RESID, gd, l + 1 < mc.n_layers, st, &pending), "down");
     }
   }
   return RV_OK;
@@ -679,14 +732,13 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   {
     Prof pf(c, RV_PROF_NORM, st);
     HIP_TRY(launch_rmsnorm(dt, c->h, nout, mc.d_model, m->norm_f, mc.rms_eps, c->lm_x, c->lm_x2, (int)S, k, shift,
-                           st),
+                           nullptr, 0, st),
             "final norm");
   }
   GemmArgs gl{};
   gl.W = m->lm_head;
   gl.X = c->lm_x;
   gl.X2 = c->lm_x2;
-  gl.ldx = mc.d_model;
   gl.M = nout;
   gl.N = mc.vocab;
   gl.K = mc.d_model;
@@ -694,7 +746,7 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   gl.ldy = mc.vocab;
   {
     Prof pf(c, RV_PROF_LMHEAD, st);
-    HIP_TRY(launch_gemm(dt, EPI_STORE, gl, st), "lm head");
+    HIP_TRY(run_gemm(dt, EPI_STORE, gl, false, st), "lm head");
   }
 
   HeadArgs ha{};
@@ -837,9 +889,14 @@ rv_status rv_debug_workspace(const rv_cache* c, int32_t which, int32_t rows, voi
   if (dst_bytes < width * rows * planes)
     return fail(RV_E_BUFFER, "destination needs %zu bytes", width * rows * planes);
   hipStream_t st = (hipStream_t)stream;
-  HIP_TRY(hipMemcpyAsync(d_dst, src, width * rows, hipMemcpyDeviceToDevice, st), "copy");
-  if (planes == 2)
-    HIP_TRY(hipMemcpyAsync((char*)d_dst + width * rows, src2, width * rows, hipMemcpyDeviceToDevice, st), "copy");
+  if (!src2) {
+    HIP_TRY(hipMemcpyAsync(d_dst, src, width * rows, hipMemcpyDeviceToDevice, st), "copy");
+    return RV_OK;
+  }
+  // operand planes are stored in tiles: convert to row-major
+  const int K = (int)(width / es);
+  HIP_TRY(launch_retile(mc.dtype, src, d_dst, rows, K, false, st), "untile");
+  if (planes == 2) HIP_TRY(launch_retile(mc.dtype, src2, (char*)d_dst + width * rows, rows, K, false, st), "untile");
   return RV_OK;
 }
 
@@ -888,21 +945,19 @@ rv_status rv_debug_linear(const rv_cache* c, int32_t layer, int32_t matrix, cons
   if (y_bytes < (size_t)M * md->N * 4) return fail(RV_E_BUFFER, "y needs %zu bytes", (size_t)M * md->N * 4);
   hipStream_t st = (hipStream_t)stream;
   const size_t plane = (size_t)M * md->K * m->es;
-  HIP_TRY(hipMemcpyAsync(xbuf, d_x, plane, hipMemcpyDeviceToDevice, st), "copy");
-  if (m->es == 2)
-    HIP_TRY(hipMemcpyAsync(xbuf2, (const char*)d_x + plane, plane, hipMemcpyDeviceToDevice, st), "copy");
+  HIP_TRY(launch_retile(mc.dtype, d_x, xbuf, M, md->K, true, st), "tile");
+  if (m->es == 2) HIP_TRY(launch_retile(mc.dtype, (const char*)d_x + plane, xbuf2, M, md->K, true, st), "tile");
   GemmArgs g{};
   g.W = W;
   g.X = xbuf;
   g.X2 = xbuf2;
-  g.ldx = md->K;
   g.M = M;
   g.N = md->N;
   g.K = md->K;
   g.Y = d_y;
   g.ldy = md->N;
   g.md = *md;
-  HIP_TRY(launch_gemm(mc.dtype, EPI_STORE_LOGICAL, g, st), "linear");
+  HIP_TRY(run_gemm(mc.dtype, EPI_STORE_LOGICAL, g, false, st), "linear");
   return RV_OK;
 }
 

@@ -60,19 +60,32 @@ template <> RV_DEV void mma_step<RV_F32>(const uint4& a, const uint4& b, f32x4_t
 // two planes, hi = bf16(x) and lo = bf16(x - hi) (x - hi is exact in fp32),
 // so an operand carries ~16 significant bits and a matmul is two MFMAs;
 // fp32 models keep x in the first plane.
-template <int DT> RV_DEV void put_operand4(void* hi, void* lo, size_t i, const f32x4_t& x);
-template <> RV_DEV void put_operand4<RV_BF16>(void* hi, void* lo, size_t i, const f32x4_t& x) {
+//
+// Operand planes are stored in MFMA B-operand tiles, the same 1 KiB tiling
+// as the packed weights with tokens in place of output rows: tile
+// (token/16, k/KT), lane (token%16) + 16*((k%KT)/VEC), VEC elements per lane.
+// A matmul wave reads one tile with one contiguous 16-byte load per lane.
+RV_DEV __host__ inline size_t operand_offset(int t, int k, int K, int es) {
+  const int vec = 16 / es, kt = 4 * vec;
+  const int kin = k % kt;
+  return (((size_t)(t >> 4) * (K / kt) + k / kt) * 64 + (t & 15) + 16 * (kin / vec)) * 16 + (size_t)(kin % vec) * es;
+}
+
+// Stores x (4 consecutive k, k % 4 == 0) of token t into the operand planes.
+template <int DT> RV_DEV void put_operand4(void* hi, void* lo, int t, int k, int K, const f32x4_t& x);
+template <> RV_DEV void put_operand4<RV_BF16>(void* hi, void* lo, int t, int k, int K, const f32x4_t& x) {
   uint16_t h[4], l[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     h[j] = f2bf(x[j]);
     l[j] = f2bf(x[j] - bf2f(h[j]));
   }
-  memcpy((uint16_t*)hi + i, h, 8);
-  memcpy((uint16_t*)lo + i, l, 8);
+  const size_t o = operand_offset(t, k, K, 2);
+  memcpy((char*)hi + o, h, 8);
+  memcpy((char*)lo + o, l, 8);
 }
-template <> RV_DEV void put_operand4<RV_F32>(void* hi, void*, size_t i, const f32x4_t& x) {
-  memcpy((float*)hi + i, &x, 16);
+template <> RV_DEV void put_operand4<RV_F32>(void* hi, void*, int t, int k, int K, const f32x4_t& x) {
+  memcpy((char*)hi + operand_offset(t, k, K, 4), &x, 16);
 }
 
 // ---------------------------------------------------------------- packing

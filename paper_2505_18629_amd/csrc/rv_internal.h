@@ -14,19 +14,22 @@ hipError_t launch_fill_f32(float* dst, float v, size_t n, hipStream_t st);
 enum EpiKind {
   EPI_STORE = 0,          // Y[t][p] = acc                        (fp32)
   EPI_RESID = 1,          // Y[t][p] += acc                       (fp32 residual stream)
-  EPI_SWIGLU = 2,         // act[t][f] = T(silu(gate) * up)       (gate/up tile pairs)
-  EPI_QKV = 3,            // rotary on q/k, q -> qbuf, k/v -> KV cache
+  EPI_SWIGLU = 2,         // act = operand(silu(gate) * up)       (gate/up tile pairs)
+  EPI_QKV = 3,            // rotary on q/k, q -> operand, k/v -> KV cache
   EPI_STORE_LOGICAL = 4,  // Y[t][logical(p)] = acc               (inspection)
+  EPI_PARTIAL = 5,        // P[kg][t][p] = partial over k-group kg (summed by the next RMSNorm)
 };
 
 struct GemmArgs {
   const void* W;      // packed matrix
-  const void* X;      // operand [rows][K]: bf16 hi plane, or fp32; rows padded to the launch's token tiles
-  const void* X2;     // bf16 lo plane (bf16 models)
-  int ldx;
+  const void* X;      // operand tiles [M/16][K/KT][64][16 B]: bf16 hi plane, or fp32;
+  const void* X2;     //   bf16 lo plane; token tiles up to the launch's token groups are read
   int M, N, K;
+  int n_tg;           // token groups of MTT*16 tokens
+  int gk;             // k-groups; (K/KT) % (4*gk) == 0
   float* Y;           // STORE / RESID / STORE_LOGICAL output, leading dim ldy
   int ldy;
+  float* P;           // PARTIAL output [gk][M][ldy]
   void* act;          // SWIGLU output operand [rows][N/2] (hi plane / fp32)
   void* act2;         // lo plane
   int ld_act;
@@ -42,7 +45,8 @@ struct GemmArgs {
   int hd, n_heads, n_kv, max_len, q_rows, k_rows;
   MatDesc md;
 };
-hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, hipStream_t st);
+// nt: row tiles per workgroup (1, 2 or 4; even for SWIGLU); mtt: token tiles (1, 2, 4).
+hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, int nt, int mtt, hipStream_t st);
 
 // ---------------------------------------------------------------- attention
 // Query rows of one pass are grouped in segments (one per sequence and
@@ -75,8 +79,14 @@ hipError_t launch_attn_combine(int dtype, const AttnArgs& a, hipStream_t st);
 // RMSNorm of rows of the fp32 residual h into matmul operands (out, out2).  With gather_k >= 0
 // the output row r = b * 2(k+1) + j reads source row b*S + j (j <= k) or
 // b*S + shift + j - (k+1) (the rows the LM head needs).
-hipError_t launch_rmsnorm(int dtype, const float* h, int rows, int d, const float* gain, float eps, void* out,
-                          void* out2, int gather_S, int gather_k, int gather_shift, hipStream_t st);
+// With P != NULL the row first takes h += sum over g < gk of P[g][row] (k-group
+// order) and writes h back (the pending partials of the previous matmul).
+hipError_t launch_rmsnorm(int dtype, float* h, int rows, int d, const float* gain, float eps, void* out,
+                          void* out2, int gather_S, int gather_k, int gather_shift, const float* P, int gk,
+                          hipStream_t st);
+
+// Converts operand planes between row-major [rows][K] and operand tiles.
+hipError_t launch_retile(int dtype, const void* src, void* dst, int rows, int K, bool to_tiles, hipStream_t st);
 
 struct PlanVerify {
   int B, S, k, n_probe, P, d, V, max_len;

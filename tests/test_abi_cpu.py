@@ -32,7 +32,7 @@ def test_status_strings(rv):
 
 
 @pytest.mark.parametrize("field,value,msg", [
-    ("head_dim", 96, "head_dim"), ("d_model", 100, "multiples of 32"), ("n_kv_heads", 3, "multiple of n_kv_heads"),
+    ("head_dim", 96, "head_dim"), ("d_model", 100, "multiples of 128"), ("n_kv_heads", 3, "multiple of n_kv_heads"),
     ("vocab", 1001, "vocab"), ("dtype", 7, "dtype"), ("rms_eps", 0.0, "rms_eps"), ("n_layers", 0, "positive"),
 ])
 def test_config_validation(rv, field, value, msg):
