@@ -79,18 +79,31 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 #pragma unroll
     for (int d = 0; d < DT; ++d) O[t][d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // K/V tiles of 64 keys are staged through registers: the next tile's loads
+  // are issued before the current tile is computed.  Keys past kend are
+  // loaded from a valid row (kend - 1) and zeroed.
+  constexpr int CHUNKS = kKB * HD / 8;
+  constexpr int PER = CHUNKS / 256;
+  uint4 kr[PER], vr[PER];
+  auto fetch = [&](int kt0) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int c = tid + u * 256;
+      const int key = min(kt0 + c / (HD / 8), kend - 1), d0 = (c % (HD / 8)) * 8;
+      kr[u] = *(const uint4*)(kbase + (size_t)key * HD + d0);
+      vr[u] = *(const uint4*)(vbase + (size_t)key * HD + d0);
+    }
+  };
+  if (kbeg < kend) fetch(kbeg);
   for (int kt0 = kbeg; kt0 < kend; kt0 += kKB) {
     __syncthreads();
-    // Stage keys [kt0, kt0 + 64) (zeros past kend): K row-major, V transposed.
-    constexpr int CHUNKS = kKB * HD / 8;
-    for (int c = tid; c < CHUNKS; c += 256) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int c = tid + u * 256;
       const int kk = c / (HD / 8), d0 = (c % (HD / 8)) * 8;
-      const int key = kt0 + kk;
-      uint4 kv = {0, 0, 0, 0}, vv = {0, 0, 0, 0};
-      if (key < kend) {
-        kv = *(const uint4*)(kbase + (size_t)key * HD + d0);
-        vv = *(const uint4*)(vbase + (size_t)key * HD + d0);
-      }
+      const bool live = kt0 + kk < kend;
+      const uint4 kv = live ? kr[u] : uint4{0, 0, 0, 0};
+      const uint4 vv = live ? vr[u] : uint4{0, 0, 0, 0};
       *(uint4*)(sK + kk * KSTR + d0) = kv;
       uint16_t ve[8];
       memcpy(ve, &vv, 16);
@@ -98,6 +111,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
       for (int j = 0; j < 8; ++j) sV[(d0 + j) * VSTR + kk] = ve[j];
     }
     __syncthreads();
+    if (kt0 + kKB < kend) fetch(kt0 + kKB);
 
 #pragma unroll
     for (int t = 0; t < 2; ++t) {

@@ -48,7 +48,10 @@ RV_DEV void lse_add(float& m, float& s, float x) {
   }
 }
 
+// One workgroup per (vocabulary chunk of 2048, fused row); each thread owns 8
+// entries and loads them all before computing.
 __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
+  constexpr int E = 8;
   const int chunk = blockIdx.x, row = blockIdx.y;  // row = b*(k+1) + i
   const int k1 = a.k + 1, b = row / k1, i = row % k1;
   const float* o = a.logits + ((size_t)b * 2 * k1 + i) * a.V;
@@ -56,16 +59,25 @@ __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
   float* z = a.z + (size_t)row * a.V;
   const float wa = a.alpha, wo = 1.0f - a.alpha;
   const int v0 = chunk * a.chunk, v1 = min(a.V, v0 + a.chunk);
+  float ov[E], rv[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int v = min(v0 + threadIdx.x + e * 256, v1 - 1);
+    ov[e] = o[v];
+    rv[e] = r[v];
+  }
   float mo = -INFINITY, so = 0.f, mr = -INFINITY, sr = 0.f, mz = -INFINITY, sz = 0.f;
   Top t{-INFINITY, 0x7fffffff, -INFINITY};
-  for (int v = v0 + threadIdx.x; v < v1; v += 256) {
-    const float ov = o[v], rv = r[v];
-    const float zo = wo * ov;
-    const float zr = wa * rv;
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int v = v0 + threadIdx.x + e * 256;
+    if (v >= v1) continue;
+    const float zo = wo * ov[e];
+    const float zr = wa * rv[e];
     const float zv = zo + zr;
     z[v] = zv;
-    lse_add(mo, so, ov);
-    lse_add(mr, sr, rv);
+    lse_add(mo, so, ov[e]);
+    lse_add(mr, sr, rv[e]);
     lse_add(mz, sz, zv);
     if (zv > t.m1) {
       t.m2 = t.m1;
@@ -109,17 +121,19 @@ __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
   }
 }
 
-// One 64-thread workgroup per sequence; lane i handles fused row i.
-__global__ __launch_bounds__(64) void k_accept(HeadArgs a) {
-  const int b = blockIdx.x, lane = threadIdx.x;
+// One 256-thread workgroup per sequence.  Wave w merges the chunk statistics
+// of fused rows w, w+4, ...: lane c takes chunks c and c+64, then the wave
+// merges lanes in a fixed butterfly order.  Thread 0 then applies the rule.
+__global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
+  const int b = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int k1 = a.k + 1, R1 = a.B * k1;
   __shared__ int xhat[RV_MAX_DRAFTS + 1];
   __shared__ float top2[RV_MAX_DRAFTS + 1];
-  if (lane < k1) {
-    const int row = b * k1 + lane;
+  for (int i = w; i < k1; i += 4) {
+    const int row = b * k1 + i;
     float m[3] = {-INFINITY, -INFINITY, -INFINITY}, s[3] = {0.f, 0.f, 0.f};
     Top t{-INFINITY, 0x7fffffff, -INFINITY};
-    for (int c = 0; c < a.nchunk; ++c) {
+    for (int c = lane; c < a.nchunk; c += 64) {
       for (int f = 0; f < 3; ++f) {
         const float* p = a.part + ((size_t)(f * R1 + row) * a.nchunk + c) * 4;
         lse_merge(m[f], s[f], p[0], p[1]);
@@ -128,13 +142,20 @@ __global__ __launch_bounds__(64) void k_accept(HeadArgs a) {
       const float* po = a.part + ((size_t)(0 * R1 + row) * a.nchunk + c) * 4;
       t = top_merge(t, Top{pz[3], __float_as_int(pz[2]), po[2]});
     }
-    for (int f = 0; f < 3; ++f) a.lse[f * R1 + row] = m[f] + logf(s[f]);
-    xhat[lane] = t.i1;
-    top2[lane] = t.m2;
-    a.argmax[row] = t.i1;
+    for (int off = 32; off > 0; off >>= 1) {
+      for (int f = 0; f < 3; ++f) lse_merge(m[f], s[f], __shfl_xor(m[f], off, 64), __shfl_xor(s[f], off, 64));
+      Top u{__shfl_xor(t.m1, off, 64), __shfl_xor(t.i1, off, 64), __shfl_xor(t.m2, off, 64)};
+      t = top_merge(t, u);
+    }
+    if (lane == 0) {
+      for (int f = 0; f < 3; ++f) a.lse[f * R1 + row] = m[f] + logf(s[f]);
+      xhat[i] = t.i1;
+      top2[i] = t.m2;
+      a.argmax[row] = t.i1;
+    }
   }
   __syncthreads();
-  if (lane != 0) return;
+  if (threadIdx.x != 0) return;
   int bad = a.seq_bad[b];
   for (int j = 0; j < a.S; ++j) bad |= a.row_bad[b * a.S + j];
   if (bad) {
@@ -170,6 +191,7 @@ __global__ __launch_bounds__(64) void k_accept(HeadArgs a) {
 }
 
 __global__ __launch_bounds__(256) void k_logprob(HeadArgs a) {
+  constexpr int E = 8;
   const int chunk = blockIdx.x, fr = blockIdx.y;  // fr = f * R1 + row
   const int k1 = a.k + 1, R1 = a.B * k1;
   const int f = fr / R1, row = fr % R1, b = row / k1, i = row % k1;
@@ -178,7 +200,14 @@ __global__ __launch_bounds__(256) void k_logprob(HeadArgs a) {
   float* dst = a.lp + (size_t)fr * a.V;
   const float l = a.lse[fr];
   const int v0 = chunk * a.chunk, v1 = min(a.V, v0 + a.chunk);
-  for (int v = v0 + threadIdx.x; v < v1; v += 256) dst[v] = src[v] - l;
+  float x[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) x[e] = src[min(v0 + (int)threadIdx.x + e * 256, v1 - 1)];
+#pragma unroll
+  for (int e = 0; e < E; ++e) {
+    const int v = v0 + threadIdx.x + e * 256;
+    if (v < v1) dst[v] = x[e] - l;
+  }
 }
 
 }  // namespace
@@ -186,7 +215,7 @@ __global__ __launch_bounds__(256) void k_logprob(HeadArgs a) {
 hipError_t launch_head(const HeadArgs& a, hipStream_t st) {
   const int R1 = a.B * (a.k + 1);
   k_fuse_stats<<<dim3(a.nchunk, R1), 256, 0, st>>>(a);
-  k_accept<<<a.B, 64, 0, st>>>(a);
+  k_accept<<<a.B, 256, 0, st>>>(a);
   k_logprob<<<dim3(a.nchunk, 3 * R1), 256, 0, st>>>(a);
   return hipGetLastError();
 }

@@ -1,16 +1,20 @@
 // Block assembly, embedding gather, RMSNorm and id-history kernels.
+#include <algorithm>
+
 #include "rv_internal.h"
 
 namespace {
 
 // ----------------------------------------------------------- RMSNorm
-// y = h * rsqrt(mean(h^2) + eps) * g, stored as a matmul operand; one
-// 256-thread workgroup per row.  Pending k-group partials of the previous
-// matmul (P, gk) are first added to h in k-group order and h is written back.
-template <int DT>
-__global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ h, int d, const float* __restrict__ gain,
-                                                 float eps, void* __restrict__ out, void* __restrict__ out2, int gS,
-                                                 int gk, int gshift, const float* __restrict__ P, int pk, int rows) {
+// y = h * rsqrt(mean(h^2) + eps) * g, stored as a matmul operand.  One
+// workgroup of d / (4 NPT) threads per row: every thread owns NPT float4s of
+// the row and issues all its loads (h and the pending k-group partials of the
+// previous matmul, added in k-group order and written back to h) before
+// using any of them.
+template <int DT, int NPT>
+__global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, const float* __restrict__ gain,
+                                                  float eps, void* __restrict__ out, void* __restrict__ out2, int gS,
+                                                  int gk, int gshift, const float* __restrict__ P, int pk, int rows) {
   const int r = blockIdx.x;
   int src = r;
   if (gk >= 0) {
@@ -18,36 +22,121 @@ __global__ __launch_bounds__(256) void k_rmsnorm(float* __restrict__ h, int d, c
     src = b * gS + (j <= gk ? j : gshift + j - (gk + 1));
   }
   float* x = h + (size_t)src * d;
-  float ss = 0.f;
-  for (int i = threadIdx.x * 4; i < d; i += 256 * 4) {
-    f32x4_t v = *(const f32x4_t*)(x + i);
-    if (P) {
-      // batches of 4 independent loads; past the last k-group the load
-      // repeats a valid partial and is weighted 0
-      for (int g0 = 0; g0 < pk; g0 += 4) {
-        f32x4_t pv[4];
+  f32x4_t v[NPT];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) pv[u] = *(const f32x4_t*)(P + ((size_t)min(g0 + u, pk - 1) * rows + src) * d + i);
+  for (int e = 0; e < NPT; ++e) v[e] = *(const f32x4_t*)(x + (threadIdx.x + e * blockDim.x) * 4);
+  if (P) {
+    for (int g0 = 0; g0 < pk; g0 += 8) {
+      f32x4_t pv[NPT][8];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) v += g0 + u < pk ? pv[u] : f32x4_t{0.f, 0.f, 0.f, 0.f};
-      }
-      *(f32x4_t*)(x + i) = v;
+      for (int e = 0; e < NPT; ++e)
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          pv[e][u] = *(const f32x4_t*)(P + ((size_t)min(g0 + u, pk - 1) * rows + src) * d +
+                                       (threadIdx.x + e * blockDim.x) * 4);
+#pragma unroll
+      for (int e = 0; e < NPT; ++e)
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[e] += g0 + u < pk ? pv[e][u] : f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
-    ss += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+#pragma unroll
+    for (int e = 0; e < NPT; ++e) *(f32x4_t*)(x + (threadIdx.x + e * blockDim.x) * 4) = v[e];
   }
+  float ss = 0.f;
+#pragma unroll
+  for (int e = 0; e < NPT; ++e) ss += v[e][0] * v[e][0] + v[e][1] * v[e][1] + v[e][2] * v[e][2] + v[e][3] * v[e][3];
   ss = wave_sum(ss);
-  __shared__ float part[4];
+  __shared__ float part[16];
+  const int nw = blockDim.x >> 6;
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = ss;
   __syncthreads();
-  const float tot = (part[0] + part[1]) + (part[2] + part[3]);
+  float tot = 0.f;
+  for (int w = 0; w < nw; ++w) tot += part[w];
   const float rs = 1.0f / sqrtf(tot / (float)d + eps);
-  for (int i = threadIdx.x * 4; i < d; i += 256 * 4) {
-    const f32x4_t v = *(const f32x4_t*)(x + i);
+#pragma unroll
+  for (int e = 0; e < NPT; ++e) {
+    const int i = (threadIdx.x + e * blockDim.x) * 4;
     const f32x4_t gg = *(const f32x4_t*)(gain + i);
     f32x4_t o;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) o[j] = v[j] * rs * gg[j];
+    for (int j = 0; j < 4; ++j) o[j] = v[e][j] * rs * gg[j];
     put_operand4<DT>(out, out2, r, i, d, o);
+  }
+}
+
+// Completes a K-split QKV projection: sums the k-group partials (physical
+// row order of the packed QKV matrix) in order, applies rotate-half rotary to
+// q and k, and writes the q operand and the K/V cache rows.  One workgroup
+// per token; a thread handles rows r0..r0+3 of a 16-row tile and their
+// rotary partners r0+8..r0+11 (r0 in {0, 4}).
+template <int DT>
+__global__ __launch_bounds__(1024) void k_qkv_finish(QkvFinish a) {
+  using TR = Tr<DT>;
+  using T = typename TR::T;
+  const int tok = blockIdx.x;
+  const int pos = a.row_pos[tok], b = a.row_seq[tok];
+  const int half = a.hd / 2;
+  const int units = a.N / 8;
+  for (int u = threadIdx.x; u < units; u += blockDim.x) {
+    const int tile = u >> 1, r0 = (u & 1) * 4;
+    const int p0 = tile * 16;
+    f32x4_t x1 = {0.f, 0.f, 0.f, 0.f}, x2 = {0.f, 0.f, 0.f, 0.f};
+    for (int g0 = 0; g0 < a.gk; g0 += 8) {
+      f32x4_t l1[8], l2[8];
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        const float* row = a.P + ((size_t)min(g0 + v, a.gk - 1) * a.M + tok) * a.N + p0;
+        l1[v] = *(const f32x4_t*)(row + r0);
+        l2[v] = *(const f32x4_t*)(row + 8 + r0);
+      }
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        if (g0 + v < a.gk) {
+          x1 += l1[v];
+          x2 += l2[v];
+        }
+      }
+    }
+    if (p0 < a.q_rows + a.k_rows) {
+      const bool is_q = p0 < a.q_rows;
+      const int rel = is_q ? p0 : p0 - a.q_rows;
+      const int head = rel / a.hd, j = (rel % a.hd) >> 4;
+      const float* cs = a.rope_cos + (size_t)pos * half + 8 * j + r0;
+      const float* sn = a.rope_sin + (size_t)pos * half + 8 * j + r0;
+      f32x4_t o1, o2;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        o1[i] = x1[i] * cs[i] - x2[i] * sn[i];
+        o2[i] = x2[i] * cs[i] + x1[i] * sn[i];
+      }
+      const int d1 = 8 * j + r0, d2 = half + 8 * j + r0;
+      if (is_q) {
+        put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + d1, a.n_heads * a.hd, o1);
+        put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + d2, a.n_heads * a.hd, o2);
+      } else {
+        T* kr = (T*)a.kc + ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd;
+        T t1[4], t2[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          t1[i] = TR::store(o1[i]);
+          t2[i] = TR::store(o2[i]);
+        }
+        memcpy(kr + d1, t1, sizeof(t1));
+        memcpy(kr + d2, t2, sizeof(t2));
+      }
+    } else {
+      const int rel = p0 - a.q_rows - a.k_rows;
+      const int head = rel / a.hd, dim = rel % a.hd;
+      T* vr = (T*)a.vc + ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim;
+      T t1[4], t2[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        t1[i] = TR::store(x1[i]);
+        t2[i] = TR::store(x2[i]);
+      }
+      memcpy(vr + r0, t1, sizeof(t1));
+      memcpy(vr + 8 + r0, t2, sizeof(t2));
+    }
   }
 }
 
@@ -144,11 +233,28 @@ __global__ __launch_bounds__(256) void k_store_ids(StoreIds s) {
 hipError_t launch_rmsnorm(int dtype, float* h, int rows, int d, const float* gain, float eps, void* out,
                           void* out2, int gS, int gk, int gshift, const float* P, int pk, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-  // partial rows are indexed by source row; the gathering form never reads partials
+  // d is a multiple of 128: one float4 per thread up to d = 4096, else two
+  const int npt = d <= 4096 ? 1 : 2;
+  const int threads = d / (4 * npt);
+  if (threads > 1024 || threads % 64) return hipErrorInvalidValue;
+#define RV_NORM(DT_, N_) \
+  k_rmsnorm<DT_, N_><<<rows, threads, 0, st>>>(h, d, gain, eps, out, out2, gS, gk, gshift, P, pk, rows)
+  if (dtype == RV_BF16) {
+    if (npt == 1) RV_NORM(RV_BF16, 1); else RV_NORM(RV_BF16, 2);
+  } else {
+    if (npt == 1) RV_NORM(RV_F32, 1); else RV_NORM(RV_F32, 2);
+  }
+#undef RV_NORM
+  return hipGetLastError();
+}
+
+hipError_t launch_qkv_finish(int dtype, const QkvFinish& a, hipStream_t st) {
+  const int units = a.N / 8;
+  const int threads = std::min(1024, (units + 63) / 64 * 64);
   if (dtype == RV_BF16)
-    k_rmsnorm<RV_BF16><<<rows, 256, 0, st>>>(h, d, gain, eps, out, out2, gS, gk, gshift, P, pk, rows);
+    k_qkv_finish<RV_BF16><<<a.M, threads, 0, st>>>(a);
   else
-    k_rmsnorm<RV_F32><<<rows, 256, 0, st>>>(h, d, gain, eps, out, out2, gS, gk, gshift, P, pk, rows);
+    k_qkv_finish<RV_F32><<<a.M, threads, 0, st>>>(a);
   return hipGetLastError();
 }
 

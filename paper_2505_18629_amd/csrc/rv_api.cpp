@@ -36,7 +36,7 @@ rv_status hip_fail(hipError_t e, const char* what) {
 constexpr size_t kAlign = 256;
 constexpr int kPrefillRows = 2048;   // rows per prefill chunk
 constexpr int kSplitsPerQuery = 8;   // partial-buffer depth per query row
-constexpr int kVocabChunk = 8192;    // vocabulary chunk of the LM-head tail
+constexpr int kVocabChunk = 2048;    // vocabulary chunk of the LM-head tail (8 entries per thread)
 constexpr int kMaxSplitK = 16;       // k-groups of a split matmul
 constexpr int kSplitRows = 64;       // matmuls with at most this many rows may split K
 
@@ -98,7 +98,7 @@ struct rv_cache {
   void *xn, *xn2, *qbuf, *qbuf2, *att, *att2, *act, *act2, *lm_x, *lm_x2;
   size_t part_entries;
   float *part_o, *part_ml;
-  float* gpart;  // k-group partials of a split matmul [kMaxSplitK][kSplitRows][d_model]
+  float* gpart;  // k-group partials of a split matmul [kMaxSplitK][kSplitRows][max(d_model, qkv rows)]
   float *logits, *z, *lp, *hpart, *lse, *margins;
   int* argmax;
   int last_k = -1;
@@ -120,6 +120,7 @@ rv_status check_config(const rv_config* c) {
   if (c->n_layers <= 0 || c->d_model <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 || c->ffn_dim <= 0 ||
       c->vocab <= 0)
     return fail(RV_E_ARG, "shape fields must be positive");
+  if (c->vocab > 64 * 2 * 2048) return fail(RV_E_ARG, "vocab must be <= 262144");
   if (c->d_model % 128 || c->ffn_dim % 128 || (c->n_heads * c->head_dim) % 128)
     return fail(RV_E_ARG, "d_model, ffn_dim and n_heads*head_dim must be multiples of 128");
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
@@ -209,7 +210,7 @@ size_t cache_layout(rv_cache* c, void* buf) {
   c->lm_x2 = cv.take<void*>((size_t)c->out_rows_cap * d * e2);
   c->part_o = cv.take<float*>(c->part_entries * hd * 4);
   c->part_ml = cv.take<float*>(c->part_entries * 2 * 4);
-  c->gpart = cv.take<float*>((size_t)kMaxSplitK * kSplitRows * d * 4);
+  c->gpart = cv.take<float*>((size_t)kMaxSplitK * kSplitRows * std::max(d, c->m->qkv.N) * 4);
   c->logits = cv.take<float*>((size_t)c->out_rows_cap * mc.vocab * 4);
   c->z = cv.take<float*>((size_t)c->r1_cap * mc.vocab * 4);
   c->lp = cv.take<float*>((size_t)3 * c->r1_cap * mc.vocab * 4);
@@ -362,8 +363,21 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     g.q_rows = m->qkv.q_rows;
     g.k_rows = m->qkv.k_rows;
     {
+      // few-row passes split K; the partials are finished (sum, rotary,
+      // q operand and KV writes) by a small per-token kernel
       Prof pf(c, RV_PROF_QKV, st);
-      HIP_TRY(run_gemm(dt, EPI_QKV, g, false, st), "qkv");
+      const GemmPlan qp = plan_gemm(dt, EPI_RESID, M, g.N, g.K, true);
+      if (qp.gk > 1) {
+        g.P = c->gpart;
+        g.ldy = g.N;
+        int gk = 1;
+        HIP_TRY(run_gemm(dt, EPI_RESID, g, true, st, &gk), "qkv");
+        QkvFinish qf{c->gpart, gk, M, g.N, g.q_rows, g.k_rows, hd, mc.n_heads, mc.n_kv_heads, c->max_len,
+                     c->row_pos, c->row_seq, c->rope_cos, c->rope_sin, c->qbuf, c->qbuf2, kc, vc};
+        HIP_TRY(launch_qkv_finish(dt, qf, st), "qkv finish");
+      } else {
+        HIP_TRY(run_gemm(dt, EPI_QKV, g, false, st), "qkv");
+      }
     }
 
     at.kc = kc;

@@ -85,6 +85,21 @@ hipError_t launch_rmsnorm(int dtype, float* h, int rows, int d, const float* gai
                           void* out2, int gather_S, int gather_k, int gather_shift, const float* P, int gk,
                           hipStream_t st);
 
+struct QkvFinish {
+  const float* P;        // [gk][M][N] partials of the packed QKV matrix (physical rows)
+  int gk, M, N;
+  int q_rows, k_rows, hd, n_heads, n_kv, max_len;
+  const int* row_pos;
+  const int* row_seq;
+  const float* rope_cos;
+  const float* rope_sin;
+  void* qbuf;
+  void* qbuf2;
+  void* kc;
+  void* vc;
+};
+hipError_t launch_qkv_finish(int dtype, const QkvFinish& a, hipStream_t st);
+
 // Converts operand planes between row-major [rows][K] and operand tiles.
 hipError_t launch_retile(int dtype, const void* src, void* dst, int rows, int K, bool to_tiles, hipStream_t st);
 
