@@ -204,7 +204,9 @@ def main():
     gbs = step_bytes / (ms * 1e-3) / 1e9
     M = w.batch * S
     gu_bytes = gateup_bytes(shape, M)
-    gu_ms = per_class["gateup"]["ms_per_launch"]
+    # the dominant kernel, launched back to back over every layer's weights
+    # in the verify pass's launch shape, HIP events around the batch
+    gu_ms = rv.rv_debug_time_matrix(v.cache, rv.RV_MAT_GATEUP, M, 4 * shape.n_layers, stream=stream)
     gu_gbs = gu_bytes / (gu_ms * 1e-3) / 1e9 if gu_ms else None
     kernel_src = os.path.join(ROOT, "paper_2505_18629_amd", "csrc", "k_gemm.hip")
 

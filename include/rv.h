@@ -208,6 +208,16 @@ rv_status rv_debug_profile_read(const rv_cache* c, int32_t kclass, double* total
 /* Fused matrices as the kernels store them. */
 enum { RV_MAT_QKV = 0, RV_MAT_O = 1, RV_MAT_GATEUP = 2, RV_MAT_DOWN = 3, RV_MAT_LM_HEAD = 4 };
 
+/* Average duration (ms) of the production kernel of one matrix class
+ * (RV_MAT_O, RV_MAT_GATEUP, RV_MAT_DOWN or RV_MAT_LM_HEAD), launched `reps`
+ * times back to back on `stream` with the launch shape and epilogue a verify
+ * pass of M rows uses, cycling through the layers' weights (so no launch
+ * re-reads cached weights), timed with HIP events around the whole batch.
+ * Reads the workspace operands as they are and overwrites workspace outputs
+ * (residual stream, logits, partials); the KV cache and the id history are
+ * untouched.  Synchronous. */
+rv_status rv_debug_time_matrix(rv_cache* c, int32_t matrix, int32_t M, int32_t reps, void* stream, float* avg_ms);
+
 /* Y[M][N] = X[M][K] . W^T with the production matrix kernel, for one stored
  * matrix (layer is ignored for RV_MAT_LM_HEAD).  Columns of Y are in logical
  * order: QKV = [q rows; k rows; v rows], GATEUP = [gate rows; up rows].

@@ -41,7 +41,7 @@ EXPORTED = [
     "rv_status_str", "rv_last_error", "rv_model_bytes", "rv_init_weights", "rv_model_free",
     "rv_cache_bytes", "rv_cache_create", "rv_cache_free", "rv_prefill_cache", "rv_verify",
     "rv_debug_output", "rv_debug_export_kv", "rv_debug_export_ids", "rv_debug_weight_bits",
-    "rv_debug_linear", "rv_debug_workspace", "rv_debug_profile", "rv_debug_profile_read",
+    "rv_debug_linear", "rv_debug_workspace", "rv_debug_profile", "rv_debug_profile_read", "rv_debug_time_matrix",
 ]
 
 
@@ -83,6 +83,7 @@ _sig = {
     "rv_debug_linear": ([_vp, _i32, _i32, _vp, _i32, _vp, _sz, _vp], ctypes.c_int),
     "rv_debug_workspace": ([_vp, _i32, _i32, _vp, _sz, _vp], ctypes.c_int),
     "rv_debug_profile": ([_vp, _i32], ctypes.c_int),
+    "rv_debug_time_matrix": ([_vp, _i32, _i32, _i32, _vp, ctypes.POINTER(ctypes.c_float)], ctypes.c_int),
     "rv_debug_profile_read": ([_vp, _i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_i32)], ctypes.c_int),
 }
 for _name, (_args, _res) in _sig.items():
@@ -222,6 +223,13 @@ def rv_debug_profile_read(cache: int, kclass: int):
     ms, n = ctypes.c_double(), _i32()
     _check(_lib.rv_debug_profile_read(cache, kclass, ctypes.byref(ms), ctypes.byref(n)))
     return ms.value, n.value
+
+
+def rv_debug_time_matrix(cache: int, matrix: int, M: int, reps: int, stream=None) -> float:
+    """Average ms of the production kernel of one matrix class (synchronous)."""
+    ms = ctypes.c_float()
+    _check(_lib.rv_debug_time_matrix(cache, matrix, M, reps, _stream(stream), ctypes.byref(ms)))
+    return ms.value
 
 
 # ------------------------------------------------------------------- buffers

@@ -18,6 +18,8 @@
 //    next RMSNorm) adds the GK partials in k-group order: deterministic, no
 //    atomics.
 //  - bf16 models multiply every weight tile by both operand planes (hi, lo).
+#include <hip/hip_ext.h>
+
 #include "rv_internal.h"
 
 namespace {
@@ -214,14 +216,25 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
   }
 }
 
+template <int DT, int NT, int MTT, int EPI>
+void launch_one(const GemmArgs& a, unsigned items, hipStream_t st) {
+  const dim3 block(kWaves * 64);
+  LaunchEvents& ev = g_launch_events;
+  if (ev.start) {
+    hipExtLaunchKernelGGL(k_gemm<DT, NT, MTT, EPI>, dim3(items), block, 0, st, ev.start, ev.stop, 0, a);
+    ev = LaunchEvents{};
+  } else {
+    k_gemm<DT, NT, MTT, EPI><<<items, block, 0, st>>>(a);
+  }
+}
+
 template <int DT, int NT, int EPI>
 hipError_t launch_nt(const GemmArgs& a, int mtt, hipStream_t st) {
   const unsigned items = (unsigned)(a.n_tg * a.gk * (a.N / (16 * NT)));
-  const dim3 block(kWaves * 64);
   switch (mtt) {
-    case 1: k_gemm<DT, NT, 1, EPI><<<items, block, 0, st>>>(a); break;
-    case 2: k_gemm<DT, NT, 2, EPI><<<items, block, 0, st>>>(a); break;
-    case 4: k_gemm<DT, NT, 4, EPI><<<items, block, 0, st>>>(a); break;
+    case 1: launch_one<DT, NT, 1, EPI>(a, items, st); break;
+    case 2: launch_one<DT, NT, 2, EPI>(a, items, st); break;
+    case 4: launch_one<DT, NT, 4, EPI>(a, items, st); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

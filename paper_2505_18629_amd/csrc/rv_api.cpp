@@ -221,12 +221,23 @@ size_t cache_layout(rv_cache* c, void* buf) {
   return align_up(cv.off, kAlign);
 }
 
+}  // namespace
+thread_local LaunchEvents g_launch_events;
+namespace {
+
 // Records a start/stop event pair around one launch when profiling is on.
+// For matrix-kernel classes the pair is attached to the kernel dispatch
+// itself (timestamps at kernel start and end); for the others it is recorded
+// on the stream before and after the launch.
 struct Prof {
   rv_cache* c;
   int cls;
   hipStream_t st;
   size_t slot = SIZE_MAX;
+  bool attached = false;
+  static bool is_matrix(int k) {
+    return k == RV_PROF_QKV || k == RV_PROF_O || k == RV_PROF_GATEUP || k == RV_PROF_DOWN || k == RV_PROF_LMHEAD;
+  }
   Prof(rv_cache* c_, int cls_, hipStream_t st_) : c(c_), cls(cls_), st(st_) {
     if (!c->prof) return;
     if (c->prof_used == c->prof_cls.size()) {
@@ -242,10 +253,24 @@ struct Prof {
     }
     slot = c->prof_used++;
     c->prof_cls[slot] = cls;
-    (void)hipEventRecord(c->prof_ev[2 * slot], st);
+    if (is_matrix(cls)) {
+      attached = true;
+      g_launch_events = LaunchEvents{c->prof_ev[2 * slot], c->prof_ev[2 * slot + 1]};
+    } else {
+      (void)hipEventRecord(c->prof_ev[2 * slot], st);
+    }
   }
   ~Prof() {
-    if (slot != SIZE_MAX) (void)hipEventRecord(c->prof_ev[2 * slot + 1], st);
+    if (slot == SIZE_MAX) return;
+    if (attached) {
+      if (g_launch_events.start) {  // no matrix kernel consumed the pair
+        (void)hipEventRecord(c->prof_ev[2 * slot], st);
+        (void)hipEventRecord(c->prof_ev[2 * slot + 1], st);
+        g_launch_events = LaunchEvents{};
+      }
+    } else {
+      (void)hipEventRecord(c->prof_ev[2 * slot + 1], st);
+    }
   }
 };
 
@@ -935,6 +960,56 @@ rv_status rv_debug_profile_read(const rv_cache* c, int32_t kclass, double* total
   }
   *total_ms = tot;
   *launches = n;
+  return RV_OK;
+}
+
+rv_status rv_debug_time_matrix(rv_cache* c, int32_t matrix, int32_t M, int32_t reps, void* stream, float* avg_ms) {
+  if (!c || !avg_ms) return fail(RV_E_ARG, "cache and avg_ms must not be NULL");
+  if (M <= 0 || M > c->rows_cap || reps <= 0) return fail(RV_E_ARG, "M must be in [1, %d], reps > 0", c->rows_cap);
+  if (matrix != RV_MAT_O && matrix != RV_MAT_GATEUP && matrix != RV_MAT_DOWN && matrix != RV_MAT_LM_HEAD)
+    return fail(RV_E_ARG, "matrix %d cannot be timed", matrix);
+  rv_model* m = c->m;
+  const rv_config& mc = m->cfg;
+  const int dt = mc.dtype, d = mc.d_model;
+  hipStream_t st = (hipStream_t)stream;
+  hipEvent_t e0, e1;
+  HIP_TRY(hipEventCreate(&e0), "event");
+  HIP_TRY(hipEventCreate(&e1), "event");
+  auto launch = [&](int rep) -> hipError_t {
+    const int l = rep % mc.n_layers;
+    GemmArgs g{};
+    g.M = M;
+    switch (matrix) {
+      case RV_MAT_O:
+        g.W = m->w_o[l]; g.X = c->att; g.X2 = c->att2; g.N = d; g.K = mc.n_heads * mc.head_dim;
+        g.Y = c->h; g.ldy = d; g.P = c->gpart;
+        return run_gemm(dt, EPI_RESID, g, true, st);
+      case RV_MAT_GATEUP:
+        g.W = m->w_gateup[l]; g.X = c->xn; g.X2 = c->xn2; g.N = m->gateup.N; g.K = d;
+        g.act = c->act; g.act2 = c->act2;
+        return run_gemm(dt, EPI_SWIGLU, g, false, st);
+      case RV_MAT_DOWN:
+        g.W = m->w_down[l]; g.X = c->act; g.X2 = c->act2; g.N = d; g.K = mc.ffn_dim;
+        g.Y = c->h; g.ldy = d; g.P = c->gpart;
+        return run_gemm(dt, EPI_RESID, g, true, st);
+      default:
+        g.W = m->lm_head; g.X = c->lm_x; g.X2 = c->lm_x2; g.N = mc.vocab; g.K = d;
+        g.Y = c->logits; g.ldy = mc.vocab;
+        return run_gemm(dt, EPI_STORE, g, false, st);
+    }
+  };
+  if (matrix == RV_MAT_LM_HEAD && M > c->out_rows_cap) return fail(RV_E_ARG, "M exceeds the LM-head rows");
+  HIP_TRY(launch(0), "warm-up launch");
+  HIP_TRY(hipEventRecord(e0, st), "event");
+  for (int r = 0; r < reps; ++r) HIP_TRY(launch(r), "timed launch");
+  HIP_TRY(hipEventRecord(e1, st), "event");
+  HIP_TRY(hipEventSynchronize(e1), "event sync");
+  float ms = 0.f;
+  HIP_TRY(hipEventElapsedTime(&ms, e0, e1), "event time");
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  *avg_ms = ms / reps;
+  c->last_k = -1;  // workspace outputs no longer describe the last verify
   return RV_OK;
 }
 

@@ -10,6 +10,14 @@ hipError_t launch_init_rowmajor(int dtype, void* dst, uint64_t tensor, size_t n,
                                 hipStream_t st);
 hipError_t launch_fill_f32(float* dst, float v, size_t n, hipStream_t st);
 
+// ---------------------------------------------------------------- profiling
+// When set, the next matrix-kernel launch on this thread records these events
+// at its own start and end (hipExtLaunchKernelGGL) and clears them.
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern thread_local LaunchEvents g_launch_events;
+
 // ---------------------------------------------------------------- matrix kernel
 enum EpiKind {
   EPI_STORE = 0,          // Y[t][p] = acc                        (fp32)
