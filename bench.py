@@ -39,7 +39,7 @@ def algorithmic_bytes(shape, lens, S, k):
     w = 2 if shape.dtype == "bf16" else 4
     layer_w = (d * (qd + 2 * kvd) + qd * d + 2 * F * d + F * d) * w
     weights = L * layer_w + V * d * w
-    kv_row = 2 * kvd * w * L
+    kv_row = 2 * kvd * 4 * L  # fp32, or a bf16 hi/lo pair per element
     kv_read = sum(int(x) - 1 for x in lens) * kv_row
     kv_write = len(lens) * S * kv_row
     return weights + kv_read + kv_write

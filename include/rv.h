@@ -57,10 +57,15 @@ enum { RV_MAX_BATCH = 256, RV_MAX_DRAFTS = 32 };
 
 /* Decoder shape.  Llama-style: pre-norm RMSNorm, rotate-half rotary, GQA
  * (query head h uses kv head h / (n_heads / n_kv_heads)), SwiGLU FFN,
- * untied LM head, no biases.  dtype is the storage type of weights, matmul
- * operands and the KV cache; accumulation is fp32.
- * Requirements: d_model, ffn_dim % 32 == 0; head_dim % 16 == 0 and <= 128;
- * n_heads % n_kv_heads == 0; vocab % 16 == 0. */
+ * untied LM head, no biases.  dtype is the storage type of the weights;
+ * accumulation is fp32.  With bf16 weights every computed value that is
+ * stored for a later matmul (norm outputs, queries, the KV cache, attention
+ * and SwiGLU outputs) is kept as the pair hi = bf16(x), lo = bf16(x - hi) of
+ * its fp32 value (about 16 significant bits), so that only the weights are
+ * rounded to bf16.
+ * Requirements: d_model, ffn_dim and n_heads*head_dim multiples of 128;
+ * head_dim 32, 64 or 128; n_heads % n_kv_heads == 0; vocab % 16 == 0 and
+ * <= 262144. */
 typedef struct {
   int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
   int32_t dtype;   /* RV_F32 or RV_BF16 */
@@ -102,7 +107,8 @@ rv_status rv_init_weights(const rv_config* cfg, uint64_t seed, void* d_buf, size
 void rv_model_free(rv_model* m);
 
 /* Bytes of device memory for a cache of `batch` sequences of up to max_len
- * positions: the KV cache [layer][b][kv_head][pos][head_dim] (dtype), the
+ * positions: the KV cache [layer][b][kv_head][pos][head_dim] (fp32; for
+ * bf16 models a bf16 hi plane plus a bf16 lo plane, value = hi + lo), the
  * token-id history [b][max_len] (int32), the rotary table and the per-call
  * workspace for blocks of up to max_block rows per sequence and up to
  * max_drafts draft tokens. */
@@ -158,8 +164,9 @@ enum {
 rv_status rv_debug_output(const rv_cache* c, int32_t which, float* d_dst, size_t dst_bytes, void* stream);
 
 /* Copies K and V of one (layer, sequence) for positions [pos0, pos0+npos)
- * into d_k and d_v, each laid out [kv_head][npos][head_dim] in dtype.
- * Asynchronous. */
+ * into d_k and d_v.  fp32 models: [kv_head][npos][head_dim] fp32 each.
+ * bf16 models: [2][kv_head][npos][head_dim] bf16 each, the hi plane then the
+ * lo plane (the cached value is hi + lo).  Asynchronous. */
 rv_status rv_debug_export_kv(const rv_cache* c, int32_t layer, int32_t seq, int32_t pos0, int32_t npos,
                              void* d_k, void* d_v, size_t dst_bytes, void* stream);
 

@@ -23,13 +23,15 @@ Precision modes:
                 implementation);
   "contract" -- fp64 arithmetic, but values are rounded where the GPU library
                 stores them: fp32 for every matmul result and the residual
-                stream; K and V to the storage dtype; and every activation
-                that feeds a matmul (norm outputs, rotated q, attention
-                probabilities and output, SwiGLU output) to its operand form.
-                For bf16 models the operand form of an fp32 value x is the
-                pair hi = bf16(x), lo = bf16(x - hi), i.e. about 16
-                significant bits; for fp32 models it is fp32.  The remaining
-                GPU-vs-oracle differences are fp32 accumulation order only.
+                stream; and every computed value that is stored for a later
+                matmul -- norm outputs, rotated q, the K/V cache, attention
+                output, SwiGLU output -- to its operand form.  For bf16
+                models the operand form of an fp32 value x is the pair
+                hi = bf16(x), lo = bf16(x - hi), about 16 significant bits;
+                for fp32 models it is fp32.  The weights are the only bf16
+                values.  The remaining GPU-vs-oracle differences are fp32
+                accumulation order and the dropped lo*lo products of the
+                attention matmuls (relative 2^-16).
 """
 from __future__ import annotations
 
@@ -181,10 +183,8 @@ class _Rounding:
         return x if self.exact else round_f32(x)
 
     def kv(self, x):
-        """K/V cache storage: the model dtype."""
-        if self.exact:
-            return x
-        return round_bf16(x) if self.bf16 else round_f32(x)
+        """K/V cache storage: the operand form (bf16 hi/lo pair, or fp32)."""
+        return self.operand(x)
 
     def operand(self, x):
         """Matmul operand form of an activation: bf16 hi/lo pair or fp32."""

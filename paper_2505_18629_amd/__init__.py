@@ -205,7 +205,8 @@ def rv_debug_weight_bits(model: int, tensor: int, flat_idx) -> np.ndarray:
 
 
 def rv_debug_linear(cache: int, layer: int, matrix: int, x, y, stream=None) -> None:
-    _check(_lib.rv_debug_linear(cache, layer, matrix, _dev(x), x.shape[0], _dev(y),
+    """x: operand rows [M][K] (fp32 models) or planes [2][M][K] (bf16 models)."""
+    _check(_lib.rv_debug_linear(cache, layer, matrix, _dev(x), x.shape[-2], _dev(y),
                                 y.numel() * y.element_size(), _stream(stream)))
 
 

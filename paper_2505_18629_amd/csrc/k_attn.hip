@@ -25,16 +25,17 @@ constexpr int kKB = 64;  // keys per LDS tile
 // O^T += V^T P^T: A = V^T (16 d x 32 keys) from a transposed LDS copy of V,
 // B = P^T taken directly from the score registers: hardware k slot j of
 // lane group g is key 4g+j (j < 4) of the first 16-key tile and key
-// 16+4g+(j-4) of the second.  P is split into bf16 hi + lo parts (two MFMAs)
-// so the product keeps ~16 significant bits of P.
+// 16+4g+(j-4) of the second.  Q, K, V and P are all (hi, lo) bf16 pairs;
+// each product is hi*hi + hi*lo + lo*hi (three MFMAs; lo*lo is ~2^-16 of
+// the result and dropped).
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   constexpr int KSTR = HD + 8;     // padded K row (elements)
   constexpr int VSTR = kKB + 8;    // padded V^T row (elements)
   constexpr int DC = HD / 32;      // d chunks for QK^T
   constexpr int DT = HD / 16;      // d tiles for PV
-  __shared__ __attribute__((aligned(16))) uint16_t sK[kKB * KSTR];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[HD * VSTR];
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kKB * KSTR];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[2][HD * VSTR];
 
   const int split = blockIdx.x, qg = blockIdx.y, grp = blockIdx.z;
   const int seg = grp / a.n_kv, kvh = grp % a.n_kv;
@@ -49,8 +50,9 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4;
   const int qd = a.n_heads * HD;
-  const uint16_t* kbase = (const uint16_t*)a.kc + (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
-  const uint16_t* vbase = (const uint16_t*)a.vc + (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
+  const size_t kvoff = (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
+  const uint16_t* kbase[2] = {(const uint16_t*)a.kc + kvoff, (const uint16_t*)a.kc2 + kvoff};
+  const uint16_t* vbase[2] = {(const uint16_t*)a.vc + kvoff, (const uint16_t*)a.vc2 + kvoff};
 
   // Queries of this wave: two 16-query tiles, hi and lo operand planes.
   uint4 qB[2][2][DC];
@@ -84,14 +86,17 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   // loaded from a valid row (kend - 1) and zeroed.
   constexpr int CHUNKS = kKB * HD / 8;
   constexpr int PER = CHUNKS / 256;
-  uint4 kr[PER], vr[PER];
+  uint4 kr[2][PER], vr[2][PER];
   auto fetch = [&](int kt0) {
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int c = tid + u * 256;
       const int key = min(kt0 + c / (HD / 8), kend - 1), d0 = (c % (HD / 8)) * 8;
-      kr[u] = *(const uint4*)(kbase + (size_t)key * HD + d0);
-      vr[u] = *(const uint4*)(vbase + (size_t)key * HD + d0);
+#pragma unroll
+      for (int pl = 0; pl < 2; ++pl) {
+        kr[pl][u] = *(const uint4*)(kbase[pl] + (size_t)key * HD + d0);
+        vr[pl][u] = *(const uint4*)(vbase[pl] + (size_t)key * HD + d0);
+      }
     }
   };
   if (kbeg < kend) fetch(kbeg);
@@ -102,13 +107,16 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
       const int c = tid + u * 256;
       const int kk = c / (HD / 8), d0 = (c % (HD / 8)) * 8;
       const bool live = kt0 + kk < kend;
-      const uint4 kv = live ? kr[u] : uint4{0, 0, 0, 0};
-      const uint4 vv = live ? vr[u] : uint4{0, 0, 0, 0};
-      *(uint4*)(sK + kk * KSTR + d0) = kv;
-      uint16_t ve[8];
-      memcpy(ve, &vv, 16);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) sV[(d0 + j) * VSTR + kk] = ve[j];
+      for (int pl = 0; pl < 2; ++pl) {
+        const uint4 kv = live ? kr[pl][u] : uint4{0, 0, 0, 0};
+        const uint4 vv = live ? vr[pl][u] : uint4{0, 0, 0, 0};
+        *(uint4*)(sK[pl] + kk * KSTR + d0) = kv;
+        uint16_t ve[8];
+        memcpy(ve, &vv, 16);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sV[pl][(d0 + j) * VSTR + kk] = ve[j];
+      }
     }
     __syncthreads();
     if (kt0 + kKB < kend) fetch(kt0 + kKB);
@@ -122,10 +130,14 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
         s[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int c = 0; c < DC; ++c) {
-          const bf16x8_t ka =
-              __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK + (16 * kt + (lane & 15)) * KSTR + 32 * c + g * 8));
-          s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, __builtin_bit_cast(bf16x8_t, qB[0][t][c]), s[kt], 0, 0, 0);
-          s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, __builtin_bit_cast(bf16x8_t, qB[1][t][c]), s[kt], 0, 0, 0);
+          const int ko = (16 * kt + (lane & 15)) * KSTR + 32 * c + g * 8;
+          const bf16x8_t kh = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK[0] + ko));
+          const bf16x8_t kl = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK[1] + ko));
+          const bf16x8_t qh = __builtin_bit_cast(bf16x8_t, qB[0][t][c]);
+          const bf16x8_t ql = __builtin_bit_cast(bf16x8_t, qB[1][t][c]);
+          s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, qh, s[kt], 0, 0, 0);
+          s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, ql, s[kt], 0, 0, 0);
+          s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kl, qh, s[kt], 0, 0, 0);
         }
       }
       float mloc = -INFINITY;
@@ -171,13 +183,17 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
         }
 #pragma unroll
         for (int d = 0; d < DT; ++d) {
-          const uint16_t* vrow = sV + (16 * d + (lane & 15)) * VSTR + 32 * c + 4 * g;
-          uint2 v0 = *(const uint2*)vrow;
-          uint2 v1 = *(const uint2*)(vrow + 16);
-          uint4 va = {v0.x, v0.y, v1.x, v1.y};
-          const bf16x8_t vb = __builtin_bit_cast(bf16x8_t, va);
-          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, phi, O[t][d], 0, 0, 0);
-          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb, plo, O[t][d], 0, 0, 0);
+          bf16x8_t vb[2];
+#pragma unroll
+          for (int pl = 0; pl < 2; ++pl) {
+            const uint16_t* vrow = sV[pl] + (16 * d + (lane & 15)) * VSTR + 32 * c + 4 * g;
+            const uint2 v0 = *(const uint2*)vrow;
+            const uint2 v1 = *(const uint2*)(vrow + 16);
+            vb[pl] = __builtin_bit_cast(bf16x8_t, uint4{v0.x, v0.y, v1.x, v1.y});
+          }
+          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[0], phi, O[t][d], 0, 0, 0);
+          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[0], plo, O[t][d], 0, 0, 0);
+          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[1], phi, O[t][d], 0, 0, 0);
         }
       }
     }

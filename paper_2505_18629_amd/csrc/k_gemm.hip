@@ -85,7 +85,6 @@ RV_DEV void epilogue(const GemmArgs& a, int tile0, int kg, int tok, int lane, f3
       if (tok >= a.M) continue;
       const int p0 = (tile0 + nt) * 16;
       const int pos = a.row_pos[tok];
-      T out[4];
       if (p0 < a.q_rows + a.k_rows) {
         const bool is_q = p0 < a.q_rows;
         const int rel = is_q ? p0 : p0 - a.q_rows;
@@ -105,18 +104,14 @@ RV_DEV void epilogue(const GemmArgs& a, int tile0, int kg, int tok, int lane, f3
         if (is_q) {
           put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + dim, a.n_heads * a.hd, rot);
         } else {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) out[i] = TR::store(rot[i]);
           const int b = a.row_seq[tok];
-          memcpy((T*)a.kc + ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim, out, sizeof(out));
+          put_kv4<DT>(a.kc, a.kc2, ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim, rot);
         }
       } else {
         const int rel = p0 - a.q_rows - a.k_rows + 4 * g;
         const int head = rel / a.hd, dim = rel % a.hd;
         const int b = a.row_seq[tok];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) out[i] = TR::store(v[nt][i]);
-        memcpy((T*)a.vc + ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim, out, sizeof(out));
+        put_kv4<DT>(a.vc, a.vc2, ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim, v[nt]);
       }
     }
   }

@@ -71,8 +71,6 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, 
 // rotary partners r0+8..r0+11 (r0 in {0, 4}).
 template <int DT>
 __global__ __launch_bounds__(1024) void k_qkv_finish(QkvFinish a) {
-  using TR = Tr<DT>;
-  using T = typename TR::T;
   const int tok = blockIdx.x;
   const int pos = a.row_pos[tok], b = a.row_seq[tok];
   const int half = a.hd / 2;
@@ -114,28 +112,16 @@ __global__ __launch_bounds__(1024) void k_qkv_finish(QkvFinish a) {
         put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + d1, a.n_heads * a.hd, o1);
         put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + d2, a.n_heads * a.hd, o2);
       } else {
-        T* kr = (T*)a.kc + ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd;
-        T t1[4], t2[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          t1[i] = TR::store(o1[i]);
-          t2[i] = TR::store(o2[i]);
-        }
-        memcpy(kr + d1, t1, sizeof(t1));
-        memcpy(kr + d2, t2, sizeof(t2));
+        const size_t kr = ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd;
+        put_kv4<DT>(a.kc, a.kc2, kr + d1, o1);
+        put_kv4<DT>(a.kc, a.kc2, kr + d2, o2);
       }
     } else {
       const int rel = p0 - a.q_rows - a.k_rows;
       const int head = rel / a.hd, dim = rel % a.hd;
-      T* vr = (T*)a.vc + ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim;
-      T t1[4], t2[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        t1[i] = TR::store(x1[i]);
-        t2[i] = TR::store(x2[i]);
-      }
-      memcpy(vr + r0, t1, sizeof(t1));
-      memcpy(vr + 8 + r0, t2, sizeof(t2));
+      const size_t vr = ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim;
+      put_kv4<DT>(a.vc, a.vc2, vr + r0, x1);
+      put_kv4<DT>(a.vc, a.vc2, vr + 8 + r0, x2);
     }
   }
 }

@@ -85,8 +85,10 @@ struct rv_cache {
   size_t bytes;
   int rows_cap, out_rows_cap, r1_cap, nchunk;
   size_t kv_layer_elems;
-  char* kc;
+  char* kc;   // K cache [layer][b][kv_head][pos][hd]: bf16 hi plane, or fp32
   char* vc;
+  char* kc2;  // bf16 lo planes (bf16 models)
+  char* vc2;
   int* ids;
   float* rope_cos;
   float* rope_sin;
@@ -181,8 +183,12 @@ size_t cache_layout(rv_cache* c, void* buf) {
   c->part_entries = (size_t)c->rows_cap * mc.n_heads * kSplitsPerQuery;
   const int nseg_cap = std::max(c->B, (int)RV_MAX_SEGS);
   Carve cv(buf);
-  c->kc = cv.take<char*>(c->kv_layer_elems * mc.n_layers * es);
-  c->vc = cv.take<char*>(c->kv_layer_elems * mc.n_layers * es);
+  // bf16 models keep K and V as hi/lo bf16 planes (the operand form)
+  const size_t kv_plane = c->kv_layer_elems * mc.n_layers * es, kv_lo = es == 2 ? kv_plane : 0;
+  c->kc = cv.take<char*>(kv_plane);
+  c->vc = cv.take<char*>(kv_plane);
+  c->kc2 = cv.take<char*>(kv_lo);
+  c->vc2 = cv.take<char*>(kv_lo);
   c->ids = cv.take<int*>((size_t)c->B * c->max_len * 4);
   c->rope_cos = cv.take<float*>((size_t)c->max_len * (hd / 2) * 4);
   c->rope_sin = cv.take<float*>((size_t)c->max_len * (hd / 2) * 4);
@@ -357,8 +363,11 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
 
   int pending = 0;  // k-groups of the last residual matmul still in c->gpart
   for (int l = 0; l < mc.n_layers; ++l) {
-    char* kc = c->kc + (size_t)l * c->kv_layer_elems * m->es;
-    char* vc = c->vc + (size_t)l * c->kv_layer_elems * m->es;
+    const size_t lo = (size_t)l * c->kv_layer_elems * m->es;
+    char* kc = c->kc + lo;
+    char* vc = c->vc + lo;
+    char* kc2 = m->es == 2 ? c->kc2 + lo : nullptr;
+    char* vc2 = m->es == 2 ? c->vc2 + lo : nullptr;
     {
       Prof pf(c, RV_PROF_NORM, st);
       HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n1[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0,
@@ -377,6 +386,8 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     g.qbuf2 = c->qbuf2;
     g.kc = kc;
     g.vc = vc;
+    g.kc2 = kc2;
+    g.vc2 = vc2;
     g.row_pos = c->row_pos;
     g.row_seq = c->row_seq;
     g.rope_cos = c->rope_cos;
@@ -398,7 +409,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
         int gk = 1;
         HIP_TRY(run_gemm(dt, EPI_RESID, g, true, st, &gk), "qkv");
         QkvFinish qf{c->gpart, gk, M, g.N, g.q_rows, g.k_rows, hd, mc.n_heads, mc.n_kv_heads, c->max_len,
-                     c->row_pos, c->row_seq, c->rope_cos, c->rope_sin, c->qbuf, c->qbuf2, kc, vc};
+                     c->row_pos, c->row_seq, c->rope_cos, c->rope_sin, c->qbuf, c->qbuf2, kc, vc, kc2, vc2};
         HIP_TRY(launch_qkv_finish(dt, qf, st), "qkv finish");
       } else {
         HIP_TRY(run_gemm(dt, EPI_QKV, g, false, st), "qkv");
@@ -407,6 +418,8 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
 
     at.kc = kc;
     at.vc = vc;
+    at.kc2 = kc2;
+    at.vc2 = vc2;
     {
       Prof pf(c, RV_PROF_ATTN, st);
       HIP_TRY(launch_attention(dt, at, qgroups, st), "attention");
@@ -848,13 +861,21 @@ rv_status rv_debug_export_kv(const rv_cache* c, int32_t layer, int32_t seq, int3
       (long long)pos0 + npos > c->max_len)
     return fail(RV_E_ARG, "layer/seq/position range outside the cache");
   const size_t es = c->m->es, hd = mc.head_dim, row = (size_t)npos * hd * es;
-  if (dst_bytes < row * mc.n_kv_heads) return fail(RV_E_BUFFER, "destination needs %zu bytes", row * mc.n_kv_heads);
+  const int planes = es == 2 ? 2 : 1;
+  const size_t plane = row * mc.n_kv_heads;
+  if (dst_bytes < plane * planes) return fail(RV_E_BUFFER, "destination needs %zu bytes", plane * planes);
   const size_t off = ((size_t)layer * c->kv_layer_elems + (size_t)seq * mc.n_kv_heads * c->max_len * hd +
                       (size_t)pos0 * hd) * es;
   const size_t spitch = (size_t)c->max_len * hd * es;
   hipStream_t st = (hipStream_t)stream;
-  HIP_TRY(hipMemcpy2DAsync(d_k, row, c->kc + off, spitch, row, mc.n_kv_heads, hipMemcpyDeviceToDevice, st), "copy");
-  HIP_TRY(hipMemcpy2DAsync(d_v, row, c->vc + off, spitch, row, mc.n_kv_heads, hipMemcpyDeviceToDevice, st), "copy");
+  for (int pl = 0; pl < planes; ++pl) {
+    const char* ks = (pl ? c->kc2 : c->kc) + off;
+    const char* vs = (pl ? c->vc2 : c->vc) + off;
+    HIP_TRY(hipMemcpy2DAsync((char*)d_k + pl * plane, row, ks, spitch, row, mc.n_kv_heads, hipMemcpyDeviceToDevice, st),
+            "copy");
+    HIP_TRY(hipMemcpy2DAsync((char*)d_v + pl * plane, row, vs, spitch, row, mc.n_kv_heads, hipMemcpyDeviceToDevice, st),
+            "copy");
+  }
   return RV_OK;
 }
 

@@ -88,6 +88,22 @@ template <> RV_DEV void put_operand4<RV_F32>(void* hi, void*, int t, int k, int 
   memcpy((char*)hi + operand_offset(t, k, K, 4), &x, 16);
 }
 
+// K/V cache rows use the same operand form, in two row-major planes.
+template <int DT> RV_DEV void put_kv4(void* hi, void* lo, size_t i, const f32x4_t& x);
+template <> RV_DEV void put_kv4<RV_BF16>(void* hi, void* lo, size_t i, const f32x4_t& x) {
+  uint16_t h[4], l[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    h[j] = f2bf(x[j]);
+    l[j] = f2bf(x[j] - bf2f(h[j]));
+  }
+  memcpy((uint16_t*)hi + i, h, 8);
+  memcpy((uint16_t*)lo + i, l, 8);
+}
+template <> RV_DEV void put_kv4<RV_F32>(void* hi, void*, size_t i, const f32x4_t& x) {
+  memcpy((float*)hi + i, &x, 16);
+}
+
 // ---------------------------------------------------------------- packing
 
 // Kinds of stored (fused) matrices.  Physical row order differs from the

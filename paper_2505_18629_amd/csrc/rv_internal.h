@@ -44,8 +44,10 @@ struct GemmArgs {
   // EPI_QKV
   void* qbuf;         // rotated q operand [rows][Hq*hd] (hi plane / fp32)
   void* qbuf2;        // lo plane
-  void* kc;           // this layer's K cache [B][Hkv][max_len][hd]
+  void* kc;           // this layer's K cache [B][Hkv][max_len][hd]: hi plane (or fp32)
   void* vc;
+  void* kc2;          // lo planes (bf16 models)
+  void* vc2;
   const int* row_pos;
   const int* row_seq;
   const float* rope_cos;  // [max_len][hd/2]
@@ -63,8 +65,10 @@ hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, int nt, int mtt, h
 struct AttnArgs {
   const void* q;        // rotated q operand [rows][Hq*hd] (hi plane / fp32)
   const void* q2;       // lo plane
-  const void* kc;       // layer base of the K cache
+  const void* kc;       // layer base of the K cache: hi plane (or fp32)
   const void* vc;
+  const void* kc2;      // lo planes (bf16 models)
+  const void* vc2;
   const int* seg_b;
   const int* seg_row0;
   const int* seg_n;
@@ -105,6 +109,8 @@ struct QkvFinish {
   void* qbuf2;
   void* kc;
   void* vc;
+  void* kc2;
+  void* vc2;
 };
 hipError_t launch_qkv_finish(int dtype, const QkvFinish& a, hipStream_t st);
 
