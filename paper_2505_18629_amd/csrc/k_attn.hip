@@ -22,18 +22,25 @@ constexpr int kKB = 64;  // keys per LDS tile
 //
 // S^T = K Q^T: A = K tile (16 keys x 32 d), B = Q^T (32 d x 16 queries), so
 // lane l holds the scores of keys 4*(l/16)+i for query l%16.
-// O^T += V^T P^T: A = V^T (16 d x 32 keys) from a transposed LDS copy of V,
-// B = P^T taken directly from the score registers: hardware k slot j of
-// lane group g is key 4g+j (j < 4) of the first 16-key tile and key
-// 16+4g+(j-4) of the second.  Q, K, V and P are all (hi, lo) bf16 pairs;
-// each product is hi*hi + hi*lo + lo*hi (three MFMAs; lo*lo is ~2^-16 of
-// the result and dropped).
+// O^T += V^T P^T: A = V^T (16 d x 32 keys), B = P^T taken directly from the
+// score registers: hardware k slot j of lane group g is key 4g+j (j < 4) of
+// the first 16-key tile of a 32-key chunk and key 16+4g+(j-4) of the second.
+// V^T is staged in LDS with its keys in that slot order, so each A operand
+// is one 16-byte LDS read.  Q, K, V and P are all (hi, lo) bf16 pairs; each
+// product is hi*hi + hi*lo + lo*hi (three MFMAs; lo*lo is ~2^-16 of the
+// result and dropped).
+//
+// Every load is unconditional: rows past the valid range are clamped to a
+// valid row, and their results are masked (scores set to -inf, so their P
+// is exactly 0 against a finite V) or not stored.
 template <int HD>
 __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   constexpr int KSTR = HD + 8;     // padded K row (elements)
   constexpr int VSTR = kKB + 8;    // padded V^T row (elements)
   constexpr int DC = HD / 32;      // d chunks for QK^T
   constexpr int DT = HD / 16;      // d tiles for PV
+  constexpr int KPER = kKB * HD / 8 / 256;     // 16-byte K chunks per thread
+  constexpr int VCOMB = 2 * 4 * (HD / 4);      // (chunk, lane group, 4-d group) V units
   __shared__ __attribute__((aligned(16))) uint16_t sK[2][kKB * KSTR];
   __shared__ __attribute__((aligned(16))) uint16_t sV[2][HD * VSTR];
 
@@ -47,12 +54,15 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   const int q_end = min(Q, q_begin + 128);
   const int kmax = pos0 + (q_end - 1) / G + 1;
   const int kbeg = split * a.ks, kend = min(kmax, kbeg + a.ks);
+  const int qpos_min = pos0 + q_begin / G;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4;
   const int qd = a.n_heads * HD;
   const size_t kvoff = (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
-  const uint16_t* kbase[2] = {(const uint16_t*)a.kc + kvoff, (const uint16_t*)a.kc2 + kvoff};
-  const uint16_t* vbase[2] = {(const uint16_t*)a.vc + kvoff, (const uint16_t*)a.vc2 + kvoff};
+  const uint16_t* kbase0 = (const uint16_t*)a.kc + kvoff;
+  const uint16_t* kbase1 = (const uint16_t*)a.kc2 + kvoff;
+  const uint16_t* vbase0 = (const uint16_t*)a.vc + kvoff;
+  const uint16_t* vbase1 = (const uint16_t*)a.vc2 + kvoff;
 
   // Queries of this wave: two 16-query tiles, hi and lo operand planes.
   uint4 qB[2][2][DC];
@@ -62,15 +72,14 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   for (int t = 0; t < 2; ++t) {
     const int q = q_begin + (2 * w + t) * 16 + (lane & 15);
     qvalid[t] = q < q_end;
-    qpos[t] = qvalid[t] ? pos0 + q / G : -1;
-    const int row = row0 + (qvalid[t] ? q / G : 0), head = kvh * G + (qvalid[t] ? q % G : 0);
+    const int qc = min(q, q_end - 1);
+    qpos[t] = pos0 + qc / G;
+    const int row = row0 + qc / G, head = kvh * G + qc % G;
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl) {
       const char* qp = (const char*)(pl ? a.q2 : a.q);
 #pragma unroll
-      for (int c = 0; c < DC; ++c)
-        qB[pl][t][c] = qvalid[t] ? *(const uint4*)(qp + operand_offset(row, head * HD + 32 * c + g * 8, qd, 2))
-                                 : uint4{0, 0, 0, 0};
+      for (int c = 0; c < DC; ++c) qB[pl][t][c] = *(const uint4*)(qp + operand_offset(row, head * HD + 32 * c + g * 8, qd, 2));
     }
   }
 
@@ -81,75 +90,110 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 #pragma unroll
     for (int d = 0; d < DT; ++d) O[t][d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // K/V tiles of 64 keys are staged through registers: the next tile's loads
-  // are issued before the current tile is computed.  Keys past kend are
-  // loaded from a valid row (kend - 1) and zeroed.
-  constexpr int CHUNKS = kKB * HD / 8;
-  constexpr int PER = CHUNKS / 256;
-  uint4 kr[2][PER], vr[2][PER];
-  auto fetch = [&](int kt0) {
-#pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int c = tid + u * 256;
-      const int key = min(kt0 + c / (HD / 8), kend - 1), d0 = (c % (HD / 8)) * 8;
-#pragma unroll
-      for (int pl = 0; pl < 2; ++pl) {
-        kr[pl][u] = *(const uint4*)(kbase[pl] + (size_t)key * HD + d0);
-        vr[pl][u] = *(const uint4*)(vbase[pl] + (size_t)key * HD + d0);
-      }
-    }
-  };
-  if (kbeg < kend) fetch(kbeg);
+  // Tile staging through registers (the next tile's loads are in flight
+  // while the current one is computed).  K: thread chunk u is key c/(HD/8),
+  // dims 8*(c%(HD/8)).  V: thread unit (chunk vc, lane group vg, dims
+  // 4*vd..4*vd+3) loads the 8 keys of that slot group, 4 dims each, and
+  // writes them transposed as 4 rows of 8 slot-ordered keys.
+  const bool vthr = tid < VCOMB;
+  const int vc = tid / (4 * (HD / 4)), vg = (tid / (HD / 4)) % 4, vd = tid % (HD / 4);
+  u32x4 kr[2][KPER];
+  uint2 vr[2][8];
+#define RV_ATTN_FETCH(KT0)                                                                         \
+  do {                                                                                             \
+    _Pragma("unroll") for (int u = 0; u < KPER; ++u) {                                             \
+      const int c_ = tid + u * 256;                                                                \
+      const int key_ = min((KT0) + c_ / (HD / 8), kend - 1), d0_ = (c_ % (HD / 8)) * 8;            \
+      kr[0][u] = *(const u32x4*)(kbase0 + (size_t)key_ * HD + d0_);                                \
+      kr[1][u] = *(const u32x4*)(kbase1 + (size_t)key_ * HD + d0_);                                \
+    }                                                                                              \
+    if (vthr) {                                                                                    \
+      _Pragma("unroll") for (int j = 0; j < 8; ++j) {                                              \
+        const int key_ = min((KT0) + 32 * vc + (j < 4 ? 4 * vg + j : 16 + 4 * vg + j - 4), kend - 1); \
+        vr[0][j] = *(const uint2*)(vbase0 + (size_t)key_ * HD + 4 * vd);                           \
+        vr[1][j] = *(const uint2*)(vbase1 + (size_t)key_ * HD + 4 * vd);                           \
+      }                                                                                            \
+    }                                                                                              \
+  } while (0)
+  if (kbeg < kend) RV_ATTN_FETCH(kbeg);
   for (int kt0 = kbeg; kt0 < kend; kt0 += kKB) {
     __syncthreads();
 #pragma unroll
-    for (int u = 0; u < PER; ++u) {
+    for (int u = 0; u < KPER; ++u) {
       const int c = tid + u * 256;
       const int kk = c / (HD / 8), d0 = (c % (HD / 8)) * 8;
-      const bool live = kt0 + kk < kend;
+      *(u32x4*)(sK[0] + kk * KSTR + d0) = kr[0][u];
+      *(u32x4*)(sK[1] + kk * KSTR + d0) = kr[1][u];
+    }
+    if (vthr) {
 #pragma unroll
-      for (int pl = 0; pl < 2; ++pl) {
-        const uint4 kv = live ? kr[pl][u] : uint4{0, 0, 0, 0};
-        const uint4 vv = live ? vr[pl][u] : uint4{0, 0, 0, 0};
-        *(uint4*)(sK[pl] + kk * KSTR + d0) = kv;
-        uint16_t ve[8];
-        memcpy(ve, &vv, 16);
+      for (int pl = 0; pl < 2; ++pl)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) sV[pl][(d0 + j) * VSTR + kk] = ve[j];
-      }
+        for (int dd = 0; dd < 4; ++dd) {
+          // element dd of each key's 4 dims: low or high half of word dd/2
+          uint32_t wv[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            const uint32_t e0 = dd < 2 ? vr[pl][2 * j].x : vr[pl][2 * j].y;
+            const uint32_t e1 = dd < 2 ? vr[pl][2 * j + 1].x : vr[pl][2 * j + 1].y;
+            wv[j] = (dd & 1) ? ((e0 >> 16) | (e1 & 0xffff0000u)) : ((e0 & 0xffffu) | (e1 << 16));
+          }
+          *(uint4*)(sV[pl] + (4 * vd + dd) * VSTR + 32 * vc + 8 * vg) = uint4{wv[0], wv[1], wv[2], wv[3]};
+        }
     }
     __syncthreads();
-    if (kt0 + kKB < kend) fetch(kt0 + kKB);
+    if (kt0 + kKB < kend) RV_ATTN_FETCH(kt0 + kKB);
 
+    // scores for 64 keys x 2 query tiles
+    f32x4_t s[2][4];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      // scores for 64 keys: 4 tiles of 16
-      f32x4_t s[4];
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) s[t][kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < DC; ++c)
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
-        s[kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        const int ko = (16 * kt + (lane & 15)) * KSTR + 32 * c + g * 8;
+        const bf16x8_t kh = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK[0] + ko));
+        const bf16x8_t kl = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK[1] + ko));
 #pragma unroll
-        for (int c = 0; c < DC; ++c) {
-          const int ko = (16 * kt + (lane & 15)) * KSTR + 32 * c + g * 8;
-          const bf16x8_t kh = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK[0] + ko));
-          const bf16x8_t kl = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK[1] + ko));
+        for (int t = 0; t < 2; ++t) {
           const bf16x8_t qh = __builtin_bit_cast(bf16x8_t, qB[0][t][c]);
           const bf16x8_t ql = __builtin_bit_cast(bf16x8_t, qB[1][t][c]);
-          s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, qh, s[kt], 0, 0, 0);
-          s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, ql, s[kt], 0, 0, 0);
-          s[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kl, qh, s[kt], 0, 0, 0);
+          s[t][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, qh, s[t][kt], 0, 0, 0);
+          s[t][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, ql, s[t][kt], 0, 0, 0);
+          s[t][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kl, qh, s[t][kt], 0, 0, 0);
         }
       }
+
+    // online softmax (log2 units).  Interior tiles (every key valid and at
+    // or before the earliest query of this workgroup) need no mask; the
+    // first tile needs no rescale of the zero accumulators.
+    const bool interior = kt0 + kKB <= kend && kt0 + kKB - 1 <= qpos_min;
+    const bool first = kt0 == kbeg;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
       float mloc = -INFINITY;
+      if (interior) {
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
+        for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = kt0 + 16 * kt + 4 * g + i;
-          const bool ok = key < kend && key <= qpos[t];
-          s[kt][i] = ok ? s[kt][i] * a.scale_log2 : -INFINITY;
-          mloc = fmaxf(mloc, s[kt][i]);
-        }
+          for (int i = 0; i < 4; ++i) {
+            s[t][kt][i] *= a.scale_log2;
+            mloc = fmaxf(mloc, s[t][kt][i]);
+          }
+      } else {
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int key = kt0 + 16 * kt + 4 * g + i;
+            const bool ok = key < kend && key <= qpos[t];
+            s[t][kt][i] = ok ? s[t][kt][i] * a.scale_log2 : -INFINITY;
+            mloc = fmaxf(mloc, s[t][kt][i]);
+          }
+      }
       mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
       mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
       const float m_new = fmaxf(m_run[t], mloc);
@@ -160,22 +204,28 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          s[kt][i] = exp2f(s[kt][i] - m_use);
-          psum += s[kt][i];
+          s[t][kt][i] = exp2f(s[t][kt][i] - m_use);
+          psum += s[t][kt][i];
         }
       psum += __shfl_xor(psum, 16, 64);
       psum += __shfl_xor(psum, 32, 64);
       l_run[t] = l_run[t] * rescale + psum;
       m_run[t] = m_new;
+      if (!first) {
 #pragma unroll
-      for (int d = 0; d < DT; ++d) O[t][d] *= rescale;
+        for (int d = 0; d < DT; ++d) O[t][d] *= rescale;
+      }
+    }
 
+    // O^T += V^T P^T with P split into hi/lo B operands
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
         bf16x8_t phi, plo;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const float p = j < 4 ? s[2 * c][j] : s[2 * c + 1][j - 4];
+          const float p = j < 4 ? s[t][2 * c][j] : s[t][2 * c + 1][j - 4];
           const uint16_t hb = f2bf(p);
           const uint16_t lb = f2bf(p - bf2f(hb));
           phi[j] = __builtin_bit_cast(__bf16, hb);
@@ -183,21 +233,17 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
         }
 #pragma unroll
         for (int d = 0; d < DT; ++d) {
-          bf16x8_t vb[2];
-#pragma unroll
-          for (int pl = 0; pl < 2; ++pl) {
-            const uint16_t* vrow = sV[pl] + (16 * d + (lane & 15)) * VSTR + 32 * c + 4 * g;
-            const uint2 v0 = *(const uint2*)vrow;
-            const uint2 v1 = *(const uint2*)(vrow + 16);
-            vb[pl] = __builtin_bit_cast(bf16x8_t, uint4{v0.x, v0.y, v1.x, v1.y});
-          }
-          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[0], phi, O[t][d], 0, 0, 0);
-          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[0], plo, O[t][d], 0, 0, 0);
-          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vb[1], phi, O[t][d], 0, 0, 0);
+          const int vo = (16 * d + (lane & 15)) * VSTR + 32 * c + 8 * g;
+          const bf16x8_t vh = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sV[0] + vo));
+          const bf16x8_t vl = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sV[1] + vo));
+          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh, phi, O[t][d], 0, 0, 0);
+          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh, plo, O[t][d], 0, 0, 0);
+          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vl, phi, O[t][d], 0, 0, 0);
         }
       }
-    }
   }
+
+#undef RV_ATTN_FETCH
 
   // Partials: lane holds O^T[d = 16*dt + 4g + i][query lane%16].
 #pragma unroll
@@ -281,14 +327,29 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a, int hd) {
   const size_t e0 = (size_t)grp * a.qmax + q;
   const int ns = min(a.nsplit, pos_q / a.ks + 1);  // splits that saw keys of this query
   const int sl = min(lane, ns - 1);
+  const int d0 = min(lane, hd - 1), d1 = min(lane + 64, hd - 1);
+  // the first 16 splits' values are loaded together with the statistics
+  constexpr int F = 16;
+  float w0[F], w1[F];
+#pragma unroll
+  for (int u = 0; u < F; ++u) {
+    const size_t e = e0 + (size_t)min(u, ns - 1) * stride;
+    w0[u] = a.part_o[e * hd + d0];
+    w1[u] = a.part_o[e * hd + d1];
+  }
   const float ms = a.part_ml[2 * (e0 + sl * stride)];
   const float ls = a.part_ml[2 * (e0 + sl * stride) + 1];
   const float M = wave_max(lane < ns ? ms : -INFINITY);
   const float f = (lane < ns && ms != -INFINITY) ? exp2f(ms - M) : 0.f;
   const float L = wave_sum(ls * f);
-  const int d0 = min(lane, hd - 1), d1 = min(lane + 64, hd - 1);
   float acc0 = 0.f, acc1 = 0.f;
-  for (int s0 = 0; s0 < ns; s0 += 8) {
+#pragma unroll
+  for (int u = 0; u < F; ++u) {
+    const float fu = u < ns ? __shfl(f, u, 64) : 0.f;
+    acc0 += w0[u] * fu;
+    acc1 += w1[u] * fu;
+  }
+  for (int s0 = F; s0 < ns; s0 += 8) {
     float v0[8], v1[8], fs[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {

@@ -8,18 +8,15 @@
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 #define RV_DEV __device__ __forceinline__
 
 // ---------------------------------------------------------------- rounding
 
-// fp32 -> bf16 bits, round to nearest even (finite values; NaN kept quiet).
-RV_DEV uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x40);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
+// fp32 -> bf16 bits, round to nearest even (gfx950 converts in hardware,
+// v_cvt_pk_bf16_f32; denormals are kept and NaN stays NaN).
+RV_DEV uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 RV_DEV float bf2f(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
 
 // Storage type traits: weights, matmul operands and KV are T; a k-step of
