@@ -10,9 +10,12 @@
 //    of K/GK).  Its 4 waves take interleaved k-steps (wave w: steps
 //    kb + w, kb + w + 4, ...) so a workgroup reads one contiguous 4 KiB span
 //    of every row tile per step.
-//  - Each wave keeps the weight and operand tiles of its next DW k-steps in
-//    flight in a register ring.  Loads retire in issue order, so both kinds
-//    share the ring depth.
+//  - Each wave keeps the weight and operand tiles of its next DEPTH k-steps
+//    in flight in a register ring.  Loads retire in issue order, so both
+//    kinds share the ring depth.
+//  - The operand tiles of a k-step are re-read (from L2) by every row group,
+//    and those reads compete with the weight stream: with 2 token tiles,
+//    8 row tiles per workgroup (ring depth 2) halve them relative to 4.
 //  - The 4 per-wave partial tiles are summed in LDS in a fixed order.  With
 //    GK > 1 the workgroup writes its fp32 partial tile and the consumer (the
 //    next RMSNorm) adds the GK partials in k-group order: deterministic, no
@@ -25,7 +28,6 @@
 namespace {
 
 constexpr int kWaves = 4;
-constexpr int kDepth = 4;
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
@@ -117,7 +119,7 @@ RV_DEV void epilogue(const GemmArgs& a, int tile0, int kg, int tok, int lane, f3
   }
 }
 
-template <int DT, int NT, int MTT, int EPI>
+template <int DT, int NT, int MTT, int EPI, int kDepth>
 __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
   using TR = Tr<DT>;
   constexpr int KT = TR::KT;
@@ -213,13 +215,14 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
 
 template <int DT, int NT, int MTT, int EPI>
 void launch_one(const GemmArgs& a, unsigned items, hipStream_t st) {
+  constexpr int kDepth = NT == 8 ? 2 : 4;
   const dim3 block(kWaves * 64);
   LaunchEvents& ev = g_launch_events;
   if (ev.start) {
-    hipExtLaunchKernelGGL(k_gemm<DT, NT, MTT, EPI>, dim3(items), block, 0, st, ev.start, ev.stop, 0, a);
+    hipExtLaunchKernelGGL(k_gemm<DT, NT, MTT, EPI, kDepth>, dim3(items), block, 0, st, ev.start, ev.stop, 0, a);
     ev = LaunchEvents{};
   } else {
-    k_gemm<DT, NT, MTT, EPI><<<items, block, 0, st>>>(a);
+    k_gemm<DT, NT, MTT, EPI, kDepth><<<items, block, 0, st>>>(a);
   }
 }
 
@@ -229,7 +232,12 @@ hipError_t launch_nt(const GemmArgs& a, int mtt, hipStream_t st) {
   switch (mtt) {
     case 1: launch_one<DT, NT, 1, EPI>(a, items, st); break;
     case 2: launch_one<DT, NT, 2, EPI>(a, items, st); break;
-    case 4: launch_one<DT, NT, 4, EPI>(a, items, st); break;
+    case 4:
+      if constexpr (NT <= 4) {
+        launch_one<DT, NT, 4, EPI>(a, items, st);
+        break;
+      }
+      return hipErrorInvalidValue;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -243,6 +251,7 @@ hipError_t launch_epi(const GemmArgs& a, int nt, int mtt, hipStream_t st) {
       break;
     case 2: return launch_nt<DT, 2, EPI>(a, mtt, st);
     case 4: return launch_nt<DT, 4, EPI>(a, mtt, st);
+    case 8: return launch_nt<DT, 8, EPI>(a, mtt, st);
   }
   return hipErrorInvalidValue;
 }

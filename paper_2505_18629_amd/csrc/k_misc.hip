@@ -14,7 +14,7 @@ namespace {
 template <int DT, int NPT>
 __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, const float* __restrict__ gain,
                                                   float eps, void* __restrict__ out, void* __restrict__ out2, int gS,
-                                                  int gk, int gshift, const float* __restrict__ P, int pk, int rows) {
+                                                  int gk, int gshift, const float* __restrict__ P, int pk, int prows) {
   const int r = blockIdx.x;
   int src = r;
   if (gk >= 0) {
@@ -32,7 +32,7 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, 
       for (int e = 0; e < NPT; ++e)
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-          pv[e][u] = *(const f32x4_t*)(P + ((size_t)min(g0 + u, pk - 1) * rows + src) * d +
+          pv[e][u] = *(const f32x4_t*)(P + ((size_t)min(g0 + u, pk - 1) * prows + src) * d +
                                        (threadIdx.x + e * blockDim.x) * 4);
 #pragma unroll
       for (int e = 0; e < NPT; ++e)
@@ -217,14 +217,15 @@ __global__ __launch_bounds__(256) void k_store_ids(StoreIds s) {
 }  // namespace
 
 hipError_t launch_rmsnorm(int dtype, float* h, int rows, int d, const float* gain, float eps, void* out,
-                          void* out2, int gS, int gk, int gshift, const float* P, int pk, hipStream_t st) {
+                          void* out2, int gS, int gk, int gshift, const float* P, int pk, int prows,
+                          hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   // d is a multiple of 128: one float4 per thread up to d = 4096, else two
   const int npt = d <= 4096 ? 1 : 2;
   const int threads = d / (4 * npt);
   if (threads > 1024 || threads % 64) return hipErrorInvalidValue;
 #define RV_NORM(DT_, N_) \
-  k_rmsnorm<DT_, N_><<<rows, threads, 0, st>>>(h, d, gain, eps, out, out2, gS, gk, gshift, P, pk, rows)
+  k_rmsnorm<DT_, N_><<<rows, threads, 0, st>>>(h, d, gain, eps, out, out2, gS, gk, gshift, P, pk, prows)
   if (dtype == RV_BF16) {
     if (npt == 1) RV_NORM(RV_BF16, 1); else RV_NORM(RV_BF16, 2);
   } else {

@@ -298,14 +298,23 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K, bool allow_split) {
   p.n_tg = (M + 16 * p.mtt - 1) / (16 * p.mtt);
   p.gk = 1;
   const int nt_min = epi == EPI_SWIGLU ? 2 : 1;
+  // Large bf16 matrices against two token tiles stream best with 8 row
+  // tiles per workgroup: half the operand re-reads per weight byte, and
+  // ~200 workgroups already saturate HBM (8B gate/up: 5.1 -> 6.0 TB/s).
+  const bool wide = dtype == RV_BF16 && p.mtt == 2 && (long long)N * K >= (32LL << 20) && N % 128 == 0;
   if (allow_split && M <= kSplitRows && N % 64 == 0) {
-    p.nt = 4;
+    p.nt = wide ? 8 : 4;
+    const int target = wide ? kTarget / 2 : kTarget;
     const int cand[] = {1, 2, 4, 7, 8, 14, 16};
     for (int gk : cand) {
       if (ksteps % (4 * gk)) continue;
       p.gk = gk;
-      if ((long long)(N / 64) * gk * p.n_tg >= kTarget) break;
+      if ((long long)(N / (16 * p.nt)) * gk * p.n_tg >= target) break;
     }
+    return p;
+  }
+  if (wide && (long long)(N / 128) * p.n_tg >= kTarget / 2) {
+    p.nt = 8;
     return p;
   }
   p.nt = 4;
@@ -325,7 +334,10 @@ hipError_t run_gemm(int dtype, int epi, GemmArgs g, bool allow_split, hipStream_
 
 // Runs every decoder layer over the current row plan (h filled, segments set).
 // qmax: queries per (segment, kv head); kmax: 1 + largest position in the plan.
-rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, hipStream_t st) {
+// With split_last the last down projection may leave k-group partials in
+// c->gpart; *pending_out then gives their count (the final norm adds them).
+rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, bool split_last, int* pending_out,
+                     hipStream_t st) {
   rv_model* m = c->m;
   const rv_config& mc = m->cfg;
   const int dt = mc.dtype, d = mc.d_model, hd = mc.head_dim;
@@ -371,7 +383,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     {
       Prof pf(c, RV_PROF_NORM, st);
       HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n1[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0,
-                             pending > 1 ? c->gpart : nullptr, pending, st),
+                             pending > 1 ? c->gpart : nullptr, pending, M, st),
               "rmsnorm");
     }
 
@@ -447,7 +459,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     {
       Prof pf(c, RV_PROF_NORM, st);
       HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n2[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0,
-                             pending > 1 ? c->gpart : nullptr, pending, st),
+                             pending > 1 ? c->gpart : nullptr, pending, M, st),
               "rmsnorm");
     }
     GemmArgs gu{};
@@ -476,11 +488,11 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, h
     gd.ldy = d;
     gd.P = c->gpart;
     {
-      // the last layer writes h directly: the LM-head norm gathers rows
       Prof pf(c, RV_PROF_DOWN, st);
-      HIP_TRY(run_gemm(dt, EPI_RESID, gd, l + 1 < mc.n_layers, st, &pending), "down");
+      HIP_TRY(run_gemm(dt, EPI_RESID, gd, split_last || l + 1 < mc.n_layers, st, &pending), "down");
     }
   }
+  if (pending_out) *pending_out = pending;
   return RV_OK;
 }
 
@@ -709,7 +721,7 @@ rv_status rv_prefill_cache(rv_cache* c, const int32_t* d_prefix_ids, int32_t ld,
       Prof pf(c, RV_PROF_PLAN, st);
       HIP_TRY(launch_plan_prefill(mc.dtype, pp, st), "prefill plan");
     }
-    rv_status s = run_layers(c, rows, nseg, max_n, kmax, st);
+    rv_status s = run_layers(c, rows, nseg, max_n, kmax, false, nullptr, st);
     if (s != RV_OK) return s;
   }
   c->last_k = -1;
@@ -775,7 +787,8 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   }
 
   const int M = c->B * (int)S;
-  rv_status s = run_layers(c, M, c->B, (int)S, kmax, st);
+  int pending = 0;
+  rv_status s = run_layers(c, M, c->B, (int)S, kmax, true, &pending, st);
   if (s != RV_OK) return s;
 
   // LM head on the 2(k+1) rows per sequence that Algorithm 1 reads.
@@ -784,7 +797,7 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   {
     Prof pf(c, RV_PROF_NORM, st);
     HIP_TRY(launch_rmsnorm(dt, c->h, nout, mc.d_model, m->norm_f, mc.rms_eps, c->lm_x, c->lm_x2, (int)S, k, shift,
-                           nullptr, 0, st),
+                           pending > 1 ? c->gpart : nullptr, pending, M, st),
             "final norm");
   }
   GemmArgs gl{};

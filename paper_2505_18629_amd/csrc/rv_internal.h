@@ -55,7 +55,8 @@ struct GemmArgs {
   int hd, n_heads, n_kv, max_len, q_rows, k_rows;
   MatDesc md;
 };
-// nt: row tiles per workgroup (1, 2 or 4; even for SWIGLU); mtt: token tiles (1, 2, 4).
+// nt: row tiles per workgroup (1, 2, 4 or 8; even for SWIGLU); mtt: token tiles (1, 2, 4;
+// 1 or 2 with nt = 8).
 hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, int nt, int mtt, hipStream_t st);
 
 // ---------------------------------------------------------------- attention
@@ -91,11 +92,12 @@ hipError_t launch_attn_combine(int dtype, const AttnArgs& a, hipStream_t st);
 // RMSNorm of rows of the fp32 residual h into matmul operands (out, out2).  With gather_k >= 0
 // the output row r = b * 2(k+1) + j reads source row b*S + j (j <= k) or
 // b*S + shift + j - (k+1) (the rows the LM head needs).
-// With P != NULL the row first takes h += sum over g < gk of P[g][row] (k-group
-// order) and writes h back (the pending partials of the previous matmul).
+// With P != NULL the source row first takes h += sum over g < gk of P[g][row]
+// (k-group order; P holds p_rows rows per k-group) and writes h back (the
+// pending partials of the previous matmul).
 hipError_t launch_rmsnorm(int dtype, float* h, int rows, int d, const float* gain, float eps, void* out,
                           void* out2, int gather_S, int gather_k, int gather_shift, const float* P, int gk,
-                          hipStream_t st);
+                          int p_rows, hipStream_t st);
 
 struct QkvFinish {
   const float* P;        // [gk][M][N] partials of the packed QKV matrix (physical rows)
