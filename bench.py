@@ -45,11 +45,47 @@ def algorithmic_bytes(shape, lens, S, k):
     return weights + kv_read + kv_write
 
 
+def algorithmic_flops(shape, lens, S, k):
+    """Matmul flops of the layers over B*S rows, the LM head over the 2(k+1)
+    rows per sequence, and attention (QK^T and PV) over the cached prefix
+    plus the causal block."""
+    d, hd, F, V, L = shape.d_model, shape.head_dim, shape.ffn_dim, shape.vocab, shape.n_layers
+    qd, kvd = shape.n_heads * hd, shape.n_kv_heads * hd
+    layer_params = d * (qd + 2 * kvd) + qd * d + 3 * F * d
+    B = len(lens)
+    flops = 2 * layer_params * B * S * L + 2 * V * d * B * 2 * (k + 1)
+    flops += sum(4 * S * qd * ((int(x) - 1) + (S + 1) / 2) for x in lens) * L
+    return flops
+
+
 def gateup_bytes(shape, M):
     """Algorithmic bytes of one gate/up launch: the weight stream plus the
     operand read (hi+lo planes) and the SwiGLU operand written."""
     d, F = shape.d_model, shape.ffn_dim
     return 2 * F * d * 2 + M * d * 4 + M * F * 4
+
+
+MFMA_PEAK_TFLOPS = 2500.0  # dense bf16
+RIDGE_FLOP_PER_BYTE = MFMA_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+
+
+def gateup_flops(shape, M):
+    """Algorithmic flops of one gate/up launch (2 per multiply-add)."""
+    return 2 * M * 2 * shape.ffn_dim * shape.d_model
+
+
+def calibrate_copy(nbytes=1 << 30, reps=3):
+    """A plain device copy of known size, for scaling rocprofv3's FETCH_SIZE
+    and WRITE_SIZE counters to bytes (run under the profiler)."""
+    import torch
+    x = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    x.fill_(1)
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration_copy_bytes": nbytes, "reps": reps}), flush=True)
 
 
 def source_hash(path):
@@ -147,11 +183,17 @@ def main():
     ap.add_argument("--workload", default="8b-bf16-b1")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=5)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a 1 GiB device copy (counter calibration under rocprofv3)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the verify pass shards by sequence "
               "across data-parallel replicas; see the design notes). Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
+
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
 
     import torch
     import paper_2505_18629_amd as rv
@@ -200,6 +242,7 @@ def main():
     rv.rv_debug_profile(v.cache, False)
 
     step_bytes = algorithmic_bytes(shape, lens, S, w.k)
+    step_flops = algorithmic_flops(shape, lens, S, w.k)
     steps_per_s = 1000.0 / ms
     gbs = step_bytes / (ms * 1e-3) / 1e9
     M = w.batch * S
@@ -208,7 +251,24 @@ def main():
     # in the verify pass's launch shape, HIP events around the batch
     gu_ms = rv.rv_debug_time_matrix(v.cache, rv.RV_MAT_GATEUP, M, 4 * shape.n_layers, stream=stream)
     gu_gbs = gu_bytes / (gu_ms * 1e-3) / 1e9 if gu_ms else None
+    gu_flops = gateup_flops(shape, M)
+    # bf16 weights: M flops per weight byte; above the ridge the kernel is MFMA-bound
+    mfma_bound = shape.dtype == "bf16" and M > RIDGE_FLOP_PER_BYTE
+    if mfma_bound:
+        achieved = gu_flops / (gu_ms * 1e-3) / 1e12 if gu_ms else None
+        roofline = {"kernel": "gate/up matmul + SwiGLU", "bound": "mfma", "achieved": achieved,
+                    "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": (achieved / MFMA_PEAK_TFLOPS) if achieved else None,
+                    "algorithmic_flops_per_launch": gu_flops, "ms_per_launch": gu_ms, "traffic": None,
+                    "hbm_gbs": gu_gbs}
+    else:
+        roofline = {"kernel": "gate/up matmul + SwiGLU", "bound": "hbm", "achieved": gu_gbs, "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s", "frac": (gu_gbs / HBM_PEAK_GBS) if gu_gbs else None,
+                    "algorithmic_bytes_per_launch": gu_bytes, "ms_per_launch": gu_ms,
+                    "traffic": None}
     kernel_src = os.path.join(ROOT, "paper_2505_18629_amd", "csrc", "k_gemm.hip")
+    if w.name == "8b-bf16-b1":
+        roofline["traffic"] = traffic_from_profiles(kernel_src)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -237,12 +297,12 @@ def main():
         "hbm_gbs": gbs,
         "hbm_frac": gbs / HBM_PEAK_GBS,
         "algorithmic_bytes_per_step": step_bytes,
+        "tflops": step_flops / (ms * 1e-3) / 1e12,
+        "mfma_frac": step_flops / (ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS,
+        "algorithmic_flops_per_step": step_flops,
         "wall_s_timed": t_wall,
         "accept_len": accept,
-        "roofline": {"kernel": "gate/up matmul + SwiGLU", "bound": "hbm", "achieved": gu_gbs, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": (gu_gbs / HBM_PEAK_GBS) if gu_gbs else None,
-                     "algorithmic_bytes_per_launch": gu_bytes, "ms_per_launch": gu_ms,
-                     "traffic": traffic_from_profiles(kernel_src)},
+        "roofline": roofline,
         "kernel_ms_per_step": {k: round(v_["ms_per_step"], 4) for k, v_ in per_class.items()},
         "cpu_baseline": cpu,
     }
