@@ -33,13 +33,17 @@ constexpr int kKB = 64;  // keys per LDS tile
 // Every load is unconditional: rows past the valid range are clamped to a
 // valid row, and their results are masked (scores set to -inf, so their P
 // is exactly 0 against a finite V) or not stored.
-template <int HD>
-__global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
+template <int HD, int NW, int TPW>
+__global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
+  static_assert(NW * TPW == 8, "a workgroup covers 128 queries");
+  constexpr int NTH = NW * 64;
   constexpr int KSTR = HD + 8;     // padded K row (elements)
   constexpr int VSTR = kKB + 8;    // padded V^T row (elements)
   constexpr int DC = HD / 32;      // d chunks for QK^T
   constexpr int DT = HD / 16;      // d tiles for PV
-  constexpr int KPER = kKB * HD / 8 / 256;     // 16-byte K chunks per thread
+  constexpr int KCH = kKB * HD / 8;            // 16-byte K chunks per tile
+  constexpr int KPER = KCH >= NTH ? KCH / NTH : 1;  // per thread
+  static_assert(KCH % NTH == 0 || NTH % KCH == 0, "K chunks must tile the workgroup");
   constexpr int VCOMB = 2 * 4 * (HD / 4);      // (chunk, lane group, 4-d group) V units
   __shared__ __attribute__((aligned(16))) uint16_t sK[2][kKB * KSTR];
   __shared__ __attribute__((aligned(16))) uint16_t sV[2][HD * VSTR];
@@ -64,13 +68,13 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   const uint16_t* vbase0 = (const uint16_t*)a.vc + kvoff;
   const uint16_t* vbase1 = (const uint16_t*)a.vc2 + kvoff;
 
-  // Queries of this wave: two 16-query tiles, hi and lo operand planes.
-  uint4 qB[2][2][DC];
-  int qpos[2];
-  bool qvalid[2];
+  // Queries of this wave: TPW 16-query tiles, hi and lo operand planes.
+  uint4 qB[2][TPW][DC];
+  int qpos[TPW];
+  bool qvalid[TPW];
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
-    const int q = q_begin + (2 * w + t) * 16 + (lane & 15);
+  for (int t = 0; t < TPW; ++t) {
+    const int q = q_begin + (TPW * w + t) * 16 + (lane & 15);
     qvalid[t] = q < q_end;
     const int qc = min(q, q_end - 1);
     qpos[t] = pos0 + qc / G;
@@ -83,10 +87,15 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
     }
   }
 
-  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
-  f32x4_t O[2][DT];
+  float m_run[TPW], l_run[TPW];
 #pragma unroll
-  for (int t = 0; t < 2; ++t)
+  for (int t = 0; t < TPW; ++t) {
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+  }
+  f32x4_t O[TPW][DT];
+#pragma unroll
+  for (int t = 0; t < TPW; ++t)
 #pragma unroll
     for (int d = 0; d < DT; ++d) O[t][d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
@@ -95,17 +104,20 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   // dims 8*(c%(HD/8)).  V: thread unit (chunk vc, lane group vg, dims
   // 4*vd..4*vd+3) loads the 8 keys of that slot group, 4 dims each, and
   // writes them transposed as 4 rows of 8 slot-ordered keys.
+  const bool kthr = KCH >= NTH || tid < KCH;  // wave-uniform (KCH is a multiple of 64)
   const bool vthr = tid < VCOMB;
   const int vc = tid / (4 * (HD / 4)), vg = (tid / (HD / 4)) % 4, vd = tid % (HD / 4);
   u32x4 kr[2][KPER];
   uint2 vr[2][8];
 #define RV_ATTN_FETCH(KT0)                                                                         \
   do {                                                                                             \
-    _Pragma("unroll") for (int u = 0; u < KPER; ++u) {                                             \
-      const int c_ = tid + u * 256;                                                                \
-      const int key_ = min((KT0) + c_ / (HD / 8), kend - 1), d0_ = (c_ % (HD / 8)) * 8;            \
-      kr[0][u] = *(const u32x4*)(kbase0 + (size_t)key_ * HD + d0_);                                \
-      kr[1][u] = *(const u32x4*)(kbase1 + (size_t)key_ * HD + d0_);                                \
+    if (kthr) {                                                                                    \
+      _Pragma("unroll") for (int u = 0; u < KPER; ++u) {                                           \
+        const int c_ = tid + u * NTH;                                                              \
+        const int key_ = min((KT0) + c_ / (HD / 8), kend - 1), d0_ = (c_ % (HD / 8)) * 8;          \
+        kr[0][u] = *(const u32x4*)(kbase0 + (size_t)key_ * HD + d0_);                              \
+        kr[1][u] = *(const u32x4*)(kbase1 + (size_t)key_ * HD + d0_);                              \
+      }                                                                                            \
     }                                                                                              \
     if (vthr) {                                                                                    \
       _Pragma("unroll") for (int j = 0; j < 8; ++j) {                                              \
@@ -118,12 +130,14 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
   if (kbeg < kend) RV_ATTN_FETCH(kbeg);
   for (int kt0 = kbeg; kt0 < kend; kt0 += kKB) {
     __syncthreads();
+    if (kthr) {
 #pragma unroll
-    for (int u = 0; u < KPER; ++u) {
-      const int c = tid + u * 256;
-      const int kk = c / (HD / 8), d0 = (c % (HD / 8)) * 8;
-      *(u32x4*)(sK[0] + kk * KSTR + d0) = kr[0][u];
-      *(u32x4*)(sK[1] + kk * KSTR + d0) = kr[1][u];
+      for (int u = 0; u < KPER; ++u) {
+        const int c = tid + u * NTH;
+        const int kk = c / (HD / 8), d0 = (c % (HD / 8)) * 8;
+        *(u32x4*)(sK[0] + kk * KSTR + d0) = kr[0][u];
+        *(u32x4*)(sK[1] + kk * KSTR + d0) = kr[1][u];
+      }
     }
     if (vthr) {
 #pragma unroll
@@ -145,9 +159,9 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
     if (kt0 + kKB < kend) RV_ATTN_FETCH(kt0 + kKB);
 
     // scores for 64 keys x 2 query tiles
-    f32x4_t s[2][4];
+    f32x4_t s[TPW][4];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < TPW; ++t)
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) s[t][kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -158,7 +172,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
         const bf16x8_t kh = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK[0] + ko));
         const bf16x8_t kl = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK[1] + ko));
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
+        for (int t = 0; t < TPW; ++t) {
           const bf16x8_t qh = __builtin_bit_cast(bf16x8_t, qB[0][t][c]);
           const bf16x8_t ql = __builtin_bit_cast(bf16x8_t, qB[1][t][c]);
           s[t][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, qh, s[t][kt], 0, 0, 0);
@@ -173,7 +187,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
     const bool interior = kt0 + kKB <= kend && kt0 + kKB - 1 <= qpos_min;
     const bool first = kt0 == kbeg;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
+    for (int t = 0; t < TPW; ++t) {
       float mloc = -INFINITY;
       if (interior) {
 #pragma unroll
@@ -221,7 +235,7 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 #pragma unroll
     for (int c = 0; c < 2; ++c)
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
+      for (int t = 0; t < TPW; ++t) {
         bf16x8_t phi, plo;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -247,9 +261,9 @@ __global__ __launch_bounds__(256) void k_attn_bf16(AttnArgs a) {
 
   // Partials: lane holds O^T[d = 16*dt + 4g + i][query lane%16].
 #pragma unroll
-  for (int t = 0; t < 2; ++t) {
+  for (int t = 0; t < TPW; ++t) {
     if (!qvalid[t]) continue;
-    const int q = q_begin + (2 * w + t) * 16 + (lane & 15);
+    const int q = q_begin + (TPW * w + t) * 16 + (lane & 15);
     const size_t e = ((size_t)split * (a.nseg * a.n_kv) + grp) * a.qmax + q;
     float* po = a.part_o + e * HD;
 #pragma unroll
@@ -390,9 +404,9 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, int n_qgroups, hipStre
   if (dtype == RV_BF16) {
     dim3 grid(a.nsplit, n_qgroups, groups);
     switch (a.hd) {
-      case 32: k_attn_bf16<32><<<grid, 256, 0, st>>>(a); break;
-      case 64: k_attn_bf16<64><<<grid, 256, 0, st>>>(a); break;
-      case 128: k_attn_bf16<128><<<grid, 256, 0, st>>>(a); break;
+      case 32: k_attn_bf16<32, 8, 1><<<grid, 512, 0, st>>>(a); break;
+      case 64: k_attn_bf16<64, 8, 1><<<grid, 512, 0, st>>>(a); break;
+      case 128: k_attn_bf16<128, 8, 1><<<grid, 512, 0, st>>>(a); break;
       default: return hipErrorInvalidValue;
     }
   } else {

@@ -213,6 +213,111 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
   }
 }
 
+// ------------------------------------------------------------ many tokens
+// bf16 only, M > 64 rows (prefill chunks, large batches).  A workgroup owns
+// BN = 4 * NT * 16 output rows x BM = MT * 16 tokens; its 4 waves split the
+// rows (NT tiles each) and share the token tiles: each k-step's operand tiles
+// (MT tiles x hi/lo) are staged once per workgroup in double-buffered LDS.
+// Weight tiles go straight to registers (each is used by one wave against all
+// MT token tiles).  Both are fetched DEPTH k-steps ahead through a register
+// ring.  Workgroups that share rows (the token groups of a row group) are
+// given indices that land on one XCD and run together, so the weights come
+// from HBM about once.  Every load index is clamped, so the pipeline has no
+// branches; rows past M are computed and not stored.
+template <int NT, int MT, int EPI>
+__global__ __launch_bounds__(kWaves * 64) void k_gemm_tiled(GemmArgs a, int n_rk) {
+  constexpr int DEPTH = 4;
+  constexpr int XU = MT * 2 * 64 / 256;  // 16-byte operand chunks per thread per k-step
+  const int lane = threadIdx.x & 63;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int ksteps = a.K / 32;
+  // Item = (row group, k-group) x token group, in an XCD-aware order
+  // (workgroup b runs on XCD b % 8).
+  const int b = blockIdx.x;
+  int rk, tg;
+  if (n_rk % 8 == 0) {
+    const int j = b / 8;
+    rk = (j / a.n_tg) * 8 + b % 8;
+    tg = j % a.n_tg;
+  } else {
+    rk = b / a.n_tg;
+    tg = b % a.n_tg;
+  }
+  const int rg = rk / a.gk, kg = rk % a.gk;
+  const int ks = ksteps / a.gk, kb = kg * ks;  // this k-group's steps
+  const int tile0 = (rg * kWaves + w) * NT;    // this wave's first row tile
+  const int last_tt = (a.M - 1) >> 4;          // last valid token tile
+
+  const uint4* wp = (const uint4*)a.W + (size_t)tile0 * ksteps * 64 + (size_t)kb * 64 + lane;
+  // operand chunk u of this thread: plane, token tile, lane slot
+  const uint4* xsrc[XU];
+#pragma unroll
+  for (int u = 0; u < XU; ++u) {
+    const int c = threadIdx.x + u * 256;
+    const int pl = c / (MT * 64), m = (c / 64) % MT, l16 = c % 64;
+    const int tt = min(tg * MT + m, last_tt);
+    xsrc[u] = (const uint4*)(pl ? a.X2 : a.X) + ((size_t)tt * ksteps + kb) * 64 + l16;
+  }
+  __shared__ u32x4 xs[2][2 * MT * 64];
+
+  f32x4_t acc[NT][MT];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[nt][mt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  u32x4 wq[DEPTH][NT], xq[DEPTH][XU];
+  auto load = [&](int slot, int step) {
+    step = min(step, ks - 1);
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) wq[slot][nt] = *(const u32x4*)(wp + ((size_t)nt * ksteps + step) * 64);
+#pragma unroll
+    for (int u = 0; u < XU; ++u) xq[slot][u] = *(const u32x4*)(xsrc[u] + (size_t)step * 64);
+  };
+  auto stage = [&](int slot, int buf) {
+#pragma unroll
+    for (int u = 0; u < XU; ++u) xs[buf][threadIdx.x + u * 256] = xq[slot][u];
+  };
+  auto compute = [&](int slot, int buf) {
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const bf16x8_t xb = __builtin_bit_cast(bf16x8_t, xs[buf][(pl * MT + mt) * 64 + lane]);
+#pragma unroll
+        for (int nt = 0; nt < NT; ++nt)
+          acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wq[slot][nt]), xb,
+                                                               acc[nt][mt], 0, 0, 0);
+      }
+  };
+
+#pragma unroll
+  for (int d = 0; d < DEPTH; ++d) load(d, d);
+  stage(0, 0);
+  __syncthreads();
+  // k-step s: operands of step s+1 go to LDS, step s is computed, step
+  // s+DEPTH is fetched into the freed ring slot.
+  for (int s0 = 0; s0 < ks; s0 += DEPTH) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) {
+      const int s = s0 + d;
+      stage((d + 1) % DEPTH, (d + 1) & 1);
+      compute(d, d & 1);
+      load(d, s + DEPTH);
+      __syncthreads();
+    }
+  }
+
+  const int tok_base = tg * MT * 16 + (lane & 15);
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    f32x4_t v[NT];
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) v[nt] = acc[nt][mt];
+    epilogue<RV_BF16, NT, EPI>(a, tile0, kg, tok_base + mt * 16, lane, v);
+  }
+}
+
 template <int DT, int NT, int MTT, int EPI>
 void launch_one(const GemmArgs& a, unsigned items, hipStream_t st) {
   constexpr int kDepth = NT == 8 ? 2 : 4;
@@ -269,7 +374,46 @@ hipError_t launch_dt(int epi, const GemmArgs& a, int nt, int mtt, hipStream_t st
   return hipErrorInvalidValue;
 }
 
+template <int NT, int MT, int EPI>
+hipError_t launch_tiled_one(const GemmArgs& a, hipStream_t st) {
+  const int n_rk = a.N / (16 * kWaves * NT) * a.gk;
+  const unsigned items = (unsigned)(n_rk * a.n_tg);
+  const dim3 block(kWaves * 64);
+  LaunchEvents& ev = g_launch_events;
+  if (ev.start) {
+    hipExtLaunchKernelGGL(k_gemm_tiled<NT, MT, EPI>, dim3(items), block, 0, st, ev.start, ev.stop, 0, a, n_rk);
+    ev = LaunchEvents{};
+  } else {
+    k_gemm_tiled<NT, MT, EPI><<<items, block, 0, st>>>(a, n_rk);
+  }
+  return hipGetLastError();
+}
+
+template <int EPI>
+hipError_t launch_tiled_epi(const GemmArgs& a, int nt, int mt, hipStream_t st) {
+  if (nt == 4 && mt == 8) return launch_tiled_one<4, 8, EPI>(a, st);
+  if (nt == 4 && mt == 4) return launch_tiled_one<4, 4, EPI>(a, st);
+  if (nt == 2 && mt == 8) return launch_tiled_one<2, 8, EPI>(a, st);
+  if (nt == 2 && mt == 4) return launch_tiled_one<2, 4, EPI>(a, st);
+  return hipErrorInvalidValue;
+}
+
 }  // namespace
+
+hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int nt, int mt, hipStream_t st) {
+  const int ksteps = a.K / 32;
+  if (a.gk < 1 || ksteps % a.gk || (ksteps / a.gk) % 4) return hipErrorInvalidValue;
+  if (a.gk > 1 && epi != EPI_PARTIAL) return hipErrorInvalidValue;
+  switch (epi) {
+    case EPI_STORE: return launch_tiled_epi<EPI_STORE>(a, nt, mt, st);
+    case EPI_RESID: return launch_tiled_epi<EPI_RESID>(a, nt, mt, st);
+    case EPI_PARTIAL: return launch_tiled_epi<EPI_PARTIAL>(a, nt, mt, st);
+    case EPI_SWIGLU: return launch_tiled_epi<EPI_SWIGLU>(a, nt, mt, st);
+    case EPI_QKV: return launch_tiled_epi<EPI_QKV>(a, nt, mt, st);
+    case EPI_STORE_LOGICAL: return launch_tiled_epi<EPI_STORE_LOGICAL>(a, nt, mt, st);
+  }
+  return hipErrorInvalidValue;
+}
 
 hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, int nt, int mtt, hipStream_t st) {
   return dtype == RV_BF16 ? launch_dt<RV_BF16>(epi, a, nt, mtt, st) : launch_dt<RV_F32>(epi, a, nt, mtt, st);

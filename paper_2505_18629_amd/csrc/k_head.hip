@@ -67,7 +67,9 @@ __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
     rv[e] = r[v];
   }
   float mo = -INFINITY, so = 0.f, mr = -INFINITY, sr = 0.f, mz = -INFINITY, sz = 0.f;
-  Top t{-INFINITY, 0x7fffffff, -INFINITY};
+  // start from a valid id, so the argmax stays in the vocabulary even if
+  // no value compares greater (NaN logits)
+  Top t{-INFINITY, v0, -INFINITY};
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int v = v0 + threadIdx.x + e * 256;
@@ -149,6 +151,7 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
     }
     if (lane == 0) {
       for (int f = 0; f < 3; ++f) a.lse[f * R1 + row] = m[f] + logf(s[f]);
+      t.i1 = min(max(t.i1, 0), a.V - 1);  // every id used as an index below is in range
       xhat[i] = t.i1;
       top2[i] = t.m2;
       a.argmax[row] = t.i1;

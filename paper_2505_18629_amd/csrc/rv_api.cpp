@@ -38,6 +38,7 @@ constexpr int kPrefillRows = 2048;   // rows per prefill chunk
 constexpr int kSplitsPerQuery = 8;   // partial-buffer depth per query row
 constexpr int kVocabChunk = 2048;    // vocabulary chunk of the LM-head tail (8 entries per thread)
 constexpr int kMaxSplitK = 16;       // k-groups of a split matmul
+constexpr int kMaxSplitTiled = 4;    // k-groups of a split many-token matmul
 constexpr int kSplitRows = 64;       // matmuls with at most this many rows may split K
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
@@ -100,7 +101,8 @@ struct rv_cache {
   void *xn, *xn2, *qbuf, *qbuf2, *att, *att2, *act, *act2, *lm_x, *lm_x2;
   size_t part_entries;
   float *part_o, *part_ml;
-  float* gpart;  // k-group partials of a split matmul [kMaxSplitK][kSplitRows][max(d_model, qkv rows)]
+  float* gpart;  // k-group partials of a split matmul [gk][rows][max(d_model, qkv rows)], gk*rows <= gpart_rows
+  int gpart_rows;
   float *logits, *z, *lp, *hpart, *lse, *margins;
   int* argmax;
   int last_k = -1;
@@ -216,7 +218,8 @@ size_t cache_layout(rv_cache* c, void* buf) {
   c->lm_x2 = cv.take<void*>((size_t)c->out_rows_cap * d * e2);
   c->part_o = cv.take<float*>(c->part_entries * hd * 4);
   c->part_ml = cv.take<float*>(c->part_entries * 2 * 4);
-  c->gpart = cv.take<float*>((size_t)kMaxSplitK * kSplitRows * std::max(d, c->m->qkv.N) * 4);
+  c->gpart_rows = std::max(kMaxSplitK * kSplitRows, kMaxSplitTiled * round_up(c->B * c->max_block, 64));
+  c->gpart = cv.take<float*>((size_t)c->gpart_rows * std::max(d, c->m->qkv.N) * 4);
   c->logits = cv.take<float*>((size_t)c->out_rows_cap * mc.vocab * 4);
   c->z = cv.take<float*>((size_t)c->r1_cap * mc.vocab * 4);
   c->lp = cv.take<float*>((size_t)3 * c->r1_cap * mc.vocab * 4);
@@ -287,16 +290,32 @@ struct Prof {
 // residual-stream outputs of few-row passes (the next RMSNorm adds the
 // partials).
 struct GemmPlan {
+  bool tiled;  // many-token kernel (launch_gemm_tiled)
   int nt, mtt, n_tg, gk;
 };
 
-GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K, bool allow_split) {
+// part_rows: capacity of the partial buffer in rows (gk * M must fit).
+GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K, bool allow_split, int part_rows) {
   constexpr int kTarget = 384;
   const int ksteps = K / (dtype == RV_BF16 ? 32 : 16);
   GemmPlan p{};
+  p.gk = 1;
+  // Many tokens (bf16): the LDS-tiled kernel streams the weights about once
+  // for all token groups; narrow matrices split K to fill the chip.
+  if (dtype == RV_BF16 && M > kSplitRows && N % 128 == 0) {
+    p.tiled = true;
+    p.nt = N % 256 == 0 ? 4 : 2;
+    p.mtt = M >= 256 ? 8 : 4;
+    p.n_tg = (M + 16 * p.mtt - 1) / (16 * p.mtt);
+    const long long items = (long long)(N / (64 * p.nt)) * p.n_tg;
+    if (allow_split)
+      while (items * p.gk < 256 && 2 * p.gk <= kMaxSplitTiled && (ksteps / (2 * p.gk)) % 4 == 0 &&
+             ksteps % (2 * p.gk) == 0 && 2 * p.gk * M <= part_rows)
+        p.gk *= 2;
+    return p;
+  }
   p.mtt = M <= 16 ? 1 : M <= 32 ? 2 : 4;
   p.n_tg = (M + 16 * p.mtt - 1) / (16 * p.mtt);
-  p.gk = 1;
   const int nt_min = epi == EPI_SWIGLU ? 2 : 1;
   // Large bf16 matrices against two token tiles stream best with 8 row
   // tiles per workgroup: half the operand re-reads per weight byte, and
@@ -307,7 +326,7 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K, bool allow_split) {
     const int target = wide ? kTarget / 2 : kTarget;
     const int cand[] = {1, 2, 4, 7, 8, 14, 16};
     for (int gk : cand) {
-      if (ksteps % (4 * gk)) continue;
+      if (ksteps % (4 * gk) || gk * M > part_rows) continue;
       p.gk = gk;
       if ((long long)(N / (16 * p.nt)) * gk * p.n_tg >= target) break;
     }
@@ -323,12 +342,15 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K, bool allow_split) {
   return p;
 }
 
-hipError_t run_gemm(int dtype, int epi, GemmArgs g, bool allow_split, hipStream_t st, int* gk_out = nullptr) {
-  const GemmPlan p = plan_gemm(dtype, epi, g.M, g.N, g.K, allow_split);
+hipError_t run_gemm(const rv_cache* c, int epi, GemmArgs g, bool allow_split, hipStream_t st,
+                    int* gk_out = nullptr) {
+  const int dtype = c->m->cfg.dtype;
+  const GemmPlan p = plan_gemm(dtype, epi, g.M, g.N, g.K, allow_split, c->gpart_rows);
   g.n_tg = p.n_tg;
   g.gk = p.gk;
   if (gk_out) *gk_out = p.gk;
   const int e = (epi == EPI_RESID && p.gk > 1) ? EPI_PARTIAL : epi;
+  if (p.tiled) return launch_gemm_tiled(e, g, p.nt, p.mtt, st);
   return launch_gemm(dtype, e, g, p.nt, p.mtt, st);
 }
 
@@ -414,17 +436,17 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, b
       // few-row passes split K; the partials are finished (sum, rotary,
       // q operand and KV writes) by a small per-token kernel
       Prof pf(c, RV_PROF_QKV, st);
-      const GemmPlan qp = plan_gemm(dt, EPI_RESID, M, g.N, g.K, true);
+      const GemmPlan qp = plan_gemm(dt, EPI_RESID, M, g.N, g.K, true, c->gpart_rows);
       if (qp.gk > 1) {
         g.P = c->gpart;
         g.ldy = g.N;
         int gk = 1;
-        HIP_TRY(run_gemm(dt, EPI_RESID, g, true, st, &gk), "qkv");
+        HIP_TRY(run_gemm(c, EPI_RESID, g, true, st, &gk), "qkv");
         QkvFinish qf{c->gpart, gk, M, g.N, g.q_rows, g.k_rows, hd, mc.n_heads, mc.n_kv_heads, c->max_len,
                      c->row_pos, c->row_seq, c->rope_cos, c->rope_sin, c->qbuf, c->qbuf2, kc, vc, kc2, vc2};
         HIP_TRY(launch_qkv_finish(dt, qf, st), "qkv finish");
       } else {
-        HIP_TRY(run_gemm(dt, EPI_QKV, g, false, st), "qkv");
+        HIP_TRY(run_gemm(c, EPI_QKV, g, false, st), "qkv");
       }
     }
 
@@ -453,7 +475,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, b
     go.P = c->gpart;
     {
       Prof pf(c, RV_PROF_O, st);
-      HIP_TRY(run_gemm(dt, EPI_RESID, go, true, st, &pending), "o-proj");
+      HIP_TRY(run_gemm(c, EPI_RESID, go, true, st, &pending), "o-proj");
     }
 
     {
@@ -474,7 +496,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, b
     gu.ld_act = mc.ffn_dim;
     {
       Prof pf(c, RV_PROF_GATEUP, st);
-      HIP_TRY(run_gemm(dt, EPI_SWIGLU, gu, false, st), "gate/up");
+      HIP_TRY(run_gemm(c, EPI_SWIGLU, gu, false, st), "gate/up");
     }
 
     GemmArgs gd{};
@@ -489,7 +511,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, b
     gd.P = c->gpart;
     {
       Prof pf(c, RV_PROF_DOWN, st);
-      HIP_TRY(run_gemm(dt, EPI_RESID, gd, split_last || l + 1 < mc.n_layers, st, &pending), "down");
+      HIP_TRY(run_gemm(c, EPI_RESID, gd, split_last || l + 1 < mc.n_layers, st, &pending), "down");
     }
   }
   if (pending_out) *pending_out = pending;
@@ -811,7 +833,7 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   gl.ldy = mc.vocab;
   {
     Prof pf(c, RV_PROF_LMHEAD, st);
-    HIP_TRY(run_gemm(dt, EPI_STORE, gl, false, st), "lm head");
+    HIP_TRY(run_gemm(c, EPI_STORE, gl, false, st), "lm head");
   }
 
   HeadArgs ha{};
@@ -1017,19 +1039,19 @@ rv_status rv_debug_time_matrix(rv_cache* c, int32_t matrix, int32_t M, int32_t r
       case RV_MAT_O:
         g.W = m->w_o[l]; g.X = c->att; g.X2 = c->att2; g.N = d; g.K = mc.n_heads * mc.head_dim;
         g.Y = c->h; g.ldy = d; g.P = c->gpart;
-        return run_gemm(dt, EPI_RESID, g, true, st);
+        return run_gemm(c, EPI_RESID, g, true, st);
       case RV_MAT_GATEUP:
         g.W = m->w_gateup[l]; g.X = c->xn; g.X2 = c->xn2; g.N = m->gateup.N; g.K = d;
         g.act = c->act; g.act2 = c->act2;
-        return run_gemm(dt, EPI_SWIGLU, g, false, st);
+        return run_gemm(c, EPI_SWIGLU, g, false, st);
       case RV_MAT_DOWN:
         g.W = m->w_down[l]; g.X = c->act; g.X2 = c->act2; g.N = d; g.K = mc.ffn_dim;
         g.Y = c->h; g.ldy = d; g.P = c->gpart;
-        return run_gemm(dt, EPI_RESID, g, true, st);
+        return run_gemm(c, EPI_RESID, g, true, st);
       default:
         g.W = m->lm_head; g.X = c->lm_x; g.X2 = c->lm_x2; g.N = mc.vocab; g.K = d;
         g.Y = c->logits; g.ldy = mc.vocab;
-        return run_gemm(dt, EPI_STORE, g, false, st);
+        return run_gemm(c, EPI_STORE, g, false, st);
     }
   };
   if (matrix == RV_MAT_LM_HEAD && M > c->out_rows_cap) return fail(RV_E_ARG, "M exceeds the LM-head rows");
@@ -1080,7 +1102,7 @@ rv_status rv_debug_linear(const rv_cache* c, int32_t layer, int32_t matrix, cons
   g.Y = d_y;
   g.ldy = md->N;
   g.md = *md;
-  HIP_TRY(run_gemm(mc.dtype, EPI_STORE_LOGICAL, g, false, st), "linear");
+  HIP_TRY(run_gemm(c, EPI_STORE_LOGICAL, g, false, st), "linear");
   return RV_OK;
 }
 
