@@ -12,6 +12,8 @@ What it computes (arXiv 2505.18629):
     o_m..o_{m+g} with m = g + |template| + 1.
   * Section 3.2, Eq. 2: p_i = softmax((1 - alpha) * o_i + alpha * r_i).
   * Appendix A, Algorithm 2 (exact-match verification), at temperature 0.
+  * Appendix A, Algorithm 3 (entropy-thresholded "typical" acceptance) with
+    a greedy bonus token.
 
 Because one causal pass produces exactly the next-token logits at every block
 position, the oracle is that definition written out: a plain Llama-style
@@ -357,9 +359,49 @@ def decision_margins(z: np.ndarray, drafts: Sequence[int], n: int, tie_eps: floa
     return ms, gap, near
 
 
+def entropy(logits: np.ndarray) -> np.ndarray:
+    """Shannon entropy in nats of softmax(logits) per row, fp64:
+    H = -sum_v p_v log p_v."""
+    lp = log_softmax(logits)
+    return -(np.exp(lp) * lp).sum(-1)
+
+
+def accept_typical(z: np.ndarray, o: np.ndarray, drafts: Sequence[int], eps: float, delta: float,
+                   entropy_of: str = "fused"):
+    """Entropy-thresholded acceptance of Algorithm 3 with a greedy bonus token.
+
+    p_i = softmax(z_i) is the fused distribution (Eq. 2).  The threshold is
+    min(eps, delta * exp(-H)), with H the entropy of p_i (entropy_of="fused")
+    or of the original target distribution softmax(o_i) ("original").  Draft
+    i is accepted while p_i(x_i) exceeds its threshold (the printed rejection
+    set has the comparison reversed; acceptance of the tokens the target finds
+    plausible is what the rule is for); n counts the leading accepted drafts
+    and t = argmax z_{n+1} (lowest id on ties).  Compared in the log domain:
+    log p_i(x_i) > min(log eps, log delta - H), which keeps eps = inf and
+    delta = 0 exact.  Returns n, t and the log-domain margins of the tested
+    drafts."""
+    k = len(drafts)
+    lpz = log_softmax(z)
+    H = entropy(z if entropy_of == "fused" else o)
+    with np.errstate(divide="ignore"):
+        log_eps, log_delta = np.log(np.float64(eps)), np.log(np.float64(delta))
+    n, margins = k, []
+    for i in range(k):
+        thr = min(log_eps, log_delta - H[i])
+        m = float(lpz[i][int(drafts[i])] - thr)
+        margins.append(m)
+        if not m > 0:
+            n = i
+            break
+    t = int(np.argmax(z[n]))
+    return n, t, margins
+
+
 def verify(shape, seed: int, history: Sequence[int], drafts: Sequence[int], probe: Sequence[int],
-           alpha: float, prefix_pos: int, mode: str = "contract") -> Dict:
-    """One verify step for one sequence (Algorithm 1 with Algorithm 2's rule)."""
+           alpha: float, prefix_pos: int, mode: str = "contract", rule: str = "greedy", eps: float = 0.09,
+           delta: float = 0.3, entropy_of: str = "fused", tie_eps: float = 1e-3) -> Dict:
+    """One verify step for one sequence: Algorithm 1's block with Algorithm
+    2's rule (rule="greedy") or Algorithm 3's (rule="typical")."""
     history = [int(t) for t in history]
     drafts = [int(t) for t in drafts]
     block, shift, orig_rows, refl_rows = reflective_block(history, drafts, probe, prefix_pos)
@@ -370,11 +412,20 @@ def verify(shape, seed: int, history: Sequence[int], drafts: Sequence[int], prob
     k = len(drafts)
     o, r = logits[: k + 1], logits[k + 1:]
     z = fuse(o, r, alpha)
-    n, t = accept_greedy(z, drafts)
-    ms, gap, near = decision_margins(z, drafts, n)
+    if rule == "greedy":
+        n, t = accept_greedy(z, drafts)
+        ms, gap, near = decision_margins(z, drafts, n, tie_eps)
+    elif rule == "typical":
+        n, t, ms = accept_typical(z, o, drafts, eps, delta, entropy_of)
+        top = np.sort(np.asarray(z[n], dtype=np.float64))[-2:]
+        gap = float(top[1] - top[0])
+        near = any(abs(m) < tie_eps for m in ms) or gap < tie_eps
+    else:
+        raise ValueError(f"unknown rule {rule}")
     return {
         "block": block, "shift": shift, "o": o, "r": r, "z": z.astype(np.float64),
         "lp_o": log_softmax(o), "lp_r": log_softmax(r), "lp_z": log_softmax(z),
+        "h_z": entropy(z), "h_o": entropy(o),
         "accept_len": n, "next_id": t, "margins": ms, "gap": gap, "near_tie": near,
     }
 

@@ -7,6 +7,7 @@ import os
 import numpy as np
 import pytest
 import scipy.special
+import scipy.stats
 
 import oracle
 import workload
@@ -134,3 +135,54 @@ def test_alpha_zero_is_standard_verification(history):
     n, t = oracle.accept_greedy(res["o"], drafts)
     assert (res["accept_len"], res["next_id"]) == (n, t)
     np.testing.assert_allclose(np.exp(res["lp_z"]).sum(-1), 1.0, atol=1e-9)
+
+
+# ------------------------------------------------------------ Algorithm 3
+
+@pytest.mark.parametrize("case", load("typical_cases.json")["cases"], ids=lambda c: c["name"])
+def test_typical_rule_golden(case):
+    o = np.array(case["o"], dtype=np.float64)
+    r = np.array(case["r"], dtype=np.float64)
+    z = oracle.fuse(o, r, case["alpha"]).astype(np.float64)
+    n, t, margins = oracle.accept_typical(z, o, case["drafts"], float(case["eps"]), float(case["delta"]),
+                                          case["entropy_of"])
+    assert (n, t) == (case["n"], case["t"])
+    # every tested draft but a rejected last one has a positive margin
+    assert all(m > 0 for m in margins[:n]) and (n == len(case["drafts"]) or margins[n] <= 0)
+
+
+def test_entropy_closed_forms():
+    # uniform over V: ln V; a two-point distribution: the binary entropy;
+    # a dominant logit: ~0; arbitrary rows: scipy's entropy of softmax
+    for V in (2, 7, 4096):
+        assert abs(oracle.entropy(np.zeros((1, V)))[0] - np.log(V)) < 1e-12
+    a = 0.3
+    h2 = -(a * np.log(a) + (1 - a) * np.log(1 - a))
+    assert abs(oracle.entropy(np.log(np.array([[a, 1 - a]])))[0] - h2) < 1e-12
+    assert oracle.entropy(np.array([[200.0, 0, 0, 0]]))[0] < 1e-80
+    rng = np.random.default_rng(3)
+    x = rng.standard_normal((6, 50)) * 2
+    ref = scipy.stats.entropy(scipy.special.softmax(x, axis=-1), axis=-1)
+    np.testing.assert_allclose(oracle.entropy(x), ref, rtol=1e-12)
+
+
+def test_typical_monotone_and_end_points():
+    rng = np.random.default_rng(11)
+    for trial in range(20):
+        k, V = 6, 40
+        # fp32-representable logits, as the fusion produces fp32
+        o = (rng.standard_normal((k + 1, V)) * 3).astype(np.float32).astype(np.float64)
+        r = (rng.standard_normal((k + 1, V)) * 3).astype(np.float32).astype(np.float64)
+        z = oracle.fuse(o, r, 0.3).astype(np.float64)
+        drafts = [int(np.argsort(z[i])[-1 - rng.integers(0, 3)]) for i in range(k)]
+        ns = [oracle.accept_typical(z, o, drafts, 0.5, d)[0] for d in (0.0, 0.05, 0.2, 0.5, 1.0, 5.0)]
+        # a larger delta raises every threshold: the accepted prefix never grows
+        assert ns == sorted(ns, reverse=True)
+        assert ns[0] == k  # delta = 0: threshold 0
+        n_all, t_all, _ = oracle.accept_typical(z, o, drafts, float("inf"), 0.0)
+        assert n_all == k and t_all == int(np.argmax(z[k]))
+        # alpha = 0: the fused rows are the original rows, so both entropy sources agree
+        z0 = oracle.fuse(o, r, 0.0).astype(np.float64)
+        for d in (0.1, 0.4):
+            assert oracle.accept_typical(z0, o, drafts, 0.3, d, "fused") == \
+                oracle.accept_typical(z0, o, drafts, 0.3, d, "original")
