@@ -52,7 +52,8 @@ typedef enum {
 } rv_status;
 
 enum { RV_F32 = 0, RV_BF16 = 1 };
-enum { RV_RULE_GREEDY = 0 };
+enum { RV_RULE_GREEDY = 0, RV_RULE_TYPICAL = 1 };
+enum { RV_ENTROPY_FUSED = 0, RV_ENTROPY_ORIGINAL = 1 };
 enum { RV_MAX_BATCH = 256, RV_MAX_DRAFTS = 32 };
 
 /* Decoder shape.  Llama-style: pre-norm RMSNorm, rotate-half rotary, GQA
@@ -74,11 +75,22 @@ typedef struct {
   float init_std;  /* std of the random-init weights, e.g. 0.02 */
 } rv_config;
 
-/* Fusion and verification parameters (Eq. 2, Table 5, Algorithm 2). */
+/* Fusion and verification parameters (Eq. 2, Table 5, Algorithms 2 and 3).
+ * RV_RULE_GREEDY (Algorithm 2 at temperature 0): draft i is accepted while
+ *   it equals argmax z_i.
+ * RV_RULE_TYPICAL (Algorithm 3): draft i is accepted while
+ *   p_i(x_i) > min(epsilon, delta * exp(-H_i)), p_i = softmax(z_i), H_i the
+ *   entropy (nats) of p_i (RV_ENTROPY_FUSED) or of softmax(o_i)
+ *   (RV_ENTROPY_ORIGINAL); compared in the log domain, so epsilon = +inf and
+ *   delta = 0 are exact.
+ * Both: n = leading accepted drafts, t = argmax z_{n+1} (lowest id on ties). */
 typedef struct {
-  float alpha;        /* weight of the reflective logits, 0 <= alpha <= 1 (Eq. 2) */
-  int32_t prefix_pos; /* P: committed tokens re-presented after the probe (Eq. 1) */
-  int32_t rule;       /* RV_RULE_GREEDY: exact match at temperature 0 (Algorithm 2) */
+  float alpha;         /* weight of the reflective logits, 0 <= alpha <= 1 (Eq. 2) */
+  int32_t prefix_pos;  /* P: committed tokens re-presented after the probe (Eq. 1) */
+  int32_t rule;        /* RV_RULE_GREEDY or RV_RULE_TYPICAL */
+  float epsilon;       /* typical: threshold cap, > 0 (may be +inf) */
+  float delta;         /* typical: entropy-scaled threshold factor, >= 0 */
+  int32_t entropy_src; /* typical: RV_ENTROPY_FUSED or RV_ENTROPY_ORIGINAL */
 } rv_fusion;
 
 typedef struct rv_model rv_model;
@@ -129,14 +141,16 @@ void rv_cache_free(rv_cache* c);
 rv_status rv_prefill_cache(rv_cache* c, const int32_t* d_prefix_ids, int32_t ld,
                            const int32_t* h_prefix_len, void* stream);
 
-/* One verification pass (Algorithm 1 with Algorithm 2's rule).
+/* One verification pass (Algorithm 1 with the rule of Algorithm 2 or 3).
  *   h_prefix_len [batch]  host: committed length L_b of each sequence;
  *                         requires max(1, P) <= L_b and L_b - 1 + S <= max_len,
  *                         S = 1 + 2k + n_probe + P <= max_block.
  *   d_draft_ids [batch][k] device int32, 0 <= k <= max_drafts.
  *   d_probe_ids [n_probe]  device int32, shared by all sequences (may be
  *                          NULL when n_probe == 0).
- *   fusion                 alpha in [0, 1], P >= 0, rule RV_RULE_GREEDY.
+ *   fusion                 alpha in [0, 1], P >= 0, rule RV_RULE_GREEDY or
+ *                          RV_RULE_TYPICAL (then epsilon > 0, delta >= 0, not
+ *                          NaN, entropy_src RV_ENTROPY_*).
  *   d_accept_len, d_next_id [batch] device int32 outputs: n_b and t_b, or
  *                          -1 and -1 if any id the block uses is out of range.
  * Side effects: writes KV at positions L_b-1 .. L_b-2+S (only L_b-1 ..
@@ -151,16 +165,23 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
 
 /* ---- inspection (tests and benchmarks) ---- */
 
-/* Which per-row result of the last rv_verify to copy.  Each is fp32
- * [batch][k+1][vocab]: raw logits o_i and r_i, fused logits z_i, and their
- * log-softmax (natural log). */
+/* Which result of the last rv_verify to copy.  RV_OUT_ORIG .. RV_OUT_LOGP_FUSED
+ * are fp32 [batch][k+1][vocab]: raw logits o_i and r_i, fused logits z_i,
+ * and their log-softmax (natural log).  RV_OUT_ENTROPY is fp32
+ * [2][batch][k+1]: the entropy (nats) of softmax(z_i), then of softmax(o_i).
+ * RV_OUT_MARGINS is fp32 [batch][k+2]: for each tested draft the distance of
+ * its decision from the boundary (greedy: z_i[x_i] - max_{v != x_i} z_i[v];
+ * typical: log p_i(x_i) - log threshold_i; NaN for untested drafts), then
+ * NaN, then the top-1 minus top-2 gap of z_{n+1}. */
 enum {
   RV_OUT_ORIG = 0, RV_OUT_REFL = 1, RV_OUT_FUSED = 2,
-  RV_OUT_LOGP_ORIG = 3, RV_OUT_LOGP_REFL = 4, RV_OUT_LOGP_FUSED = 5
+  RV_OUT_LOGP_ORIG = 3, RV_OUT_LOGP_REFL = 4, RV_OUT_LOGP_FUSED = 5,
+  RV_OUT_ENTROPY = 6, RV_OUT_MARGINS = 7
 };
 
-/* Copies one result of the last verify into d_dst (>= batch*(k+1)*vocab*4
- * bytes).  RV_E_STATE if no verify ran on this cache. Asynchronous. */
+/* Copies one result of the last verify into d_dst (at least the byte size
+ * of that result).  RV_E_STATE if no verify ran on this cache.
+ * Asynchronous. */
 rv_status rv_debug_output(const rv_cache* c, int32_t which, float* d_dst, size_t dst_bytes, void* stream);
 
 /* Copies K and V of one (layer, sequence) for positions [pos0, pos0+npos)

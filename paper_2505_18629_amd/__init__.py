@@ -28,9 +28,11 @@ import torch  # noqa: E402,F401
 _lib = ctypes.CDLL(LIB_PATH)
 
 RV_F32, RV_BF16 = 0, 1
-RV_RULE_GREEDY = 0
+RV_RULE_GREEDY, RV_RULE_TYPICAL = 0, 1
+RV_ENTROPY_FUSED, RV_ENTROPY_ORIGINAL = 0, 1
 RV_MAX_BATCH, RV_MAX_DRAFTS = 256, 32
-RV_OUT_ORIG, RV_OUT_REFL, RV_OUT_FUSED, RV_OUT_LOGP_ORIG, RV_OUT_LOGP_REFL, RV_OUT_LOGP_FUSED = range(6)
+(RV_OUT_ORIG, RV_OUT_REFL, RV_OUT_FUSED, RV_OUT_LOGP_ORIG, RV_OUT_LOGP_REFL, RV_OUT_LOGP_FUSED, RV_OUT_ENTROPY,
+ RV_OUT_MARGINS) = range(8)
 RV_MAT_QKV, RV_MAT_O, RV_MAT_GATEUP, RV_MAT_DOWN, RV_MAT_LM_HEAD = range(5)
 RV_WS_RESID, RV_WS_ATTN, RV_WS_ACT, RV_WS_QUERY = range(4)
 PROF_CLASSES = ["plan", "norm", "qkv", "attn", "combine", "o", "gateup", "down", "lmhead", "tail"]
@@ -53,7 +55,8 @@ class rv_config(ctypes.Structure):
 
 
 class rv_fusion(ctypes.Structure):
-    _fields_ = [("alpha", ctypes.c_float), ("prefix_pos", ctypes.c_int32), ("rule", ctypes.c_int32)]
+    _fields_ = [("alpha", ctypes.c_float), ("prefix_pos", ctypes.c_int32), ("rule", ctypes.c_int32),
+                ("epsilon", ctypes.c_float), ("delta", ctypes.c_float), ("entropy_src", ctypes.c_int32)]
 
 
 class RVError(RuntimeError):
@@ -176,9 +179,10 @@ def rv_prefill_cache(cache: int, prefix_ids, prefix_len: Sequence[int], stream=N
 
 
 def rv_verify(cache: int, prefix_len: Sequence[int], draft_ids, k: int, probe_ids, n_probe: int, alpha: float,
-              prefix_pos: int, accept_len, next_id, rule: int = RV_RULE_GREEDY, stream=None) -> None:
+              prefix_pos: int, accept_len, next_id, rule: int = RV_RULE_GREEDY, stream=None,
+              epsilon: float = 0.09, delta: float = 0.3, entropy_src: int = RV_ENTROPY_FUSED) -> None:
     _keep, lens = _host_i32(prefix_len)
-    fu = rv_fusion(alpha, prefix_pos, rule)
+    fu = rv_fusion(alpha, prefix_pos, rule, epsilon, delta, entropy_src)
     _check(_lib.rv_verify(cache, lens, _dev(draft_ids), k, _dev(probe_ids), n_probe, ctypes.byref(fu),
                           _dev(accept_len), _dev(next_id), _stream(stream)))
 
@@ -268,7 +272,8 @@ class Verifier:
         self._keep = d_ids
         return lens
 
-    def verify(self, prefix_len, drafts, probe, alpha: float, prefix_pos: int):
+    def verify(self, prefix_len, drafts, probe, alpha: float, prefix_pos: int, rule: int = RV_RULE_GREEDY,
+               epsilon: float = 0.09, delta: float = 0.3, entropy_src: int = RV_ENTROPY_FUSED):
         torch = self.torch
         drafts = np.asarray(drafts, dtype=np.int32).reshape(self.batch, -1)
         k = drafts.shape[1]
@@ -276,14 +281,20 @@ class Verifier:
         probe = np.asarray(probe, dtype=np.int32)
         d_pr = torch.from_numpy(probe).cuda() if len(probe) else None
         rv_verify(self.cache, prefix_len, d_dr, k, d_pr, len(probe), alpha, prefix_pos,
-                  self.accept_len, self.next_id)
+                  self.accept_len, self.next_id, rule=rule, epsilon=epsilon, delta=delta, entropy_src=entropy_src)
         self._keep2 = (d_dr, d_pr)
         self.k = k
         return self.accept_len, self.next_id
 
     def output(self, which: int):
         torch = self.torch
-        out = torch.empty((self.batch, self.k + 1, self.shape.vocab), dtype=torch.float32, device="cuda")
+        if which == RV_OUT_ENTROPY:
+            shape = (2, self.batch, self.k + 1)
+        elif which == RV_OUT_MARGINS:
+            shape = (self.batch, self.k + 2)
+        else:
+            shape = (self.batch, self.k + 1, self.shape.vocab)
+        out = torch.empty(shape, dtype=torch.float32, device="cuda")
         rv_debug_output(self.cache, which, out)
         return out
 

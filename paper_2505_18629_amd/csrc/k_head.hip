@@ -2,12 +2,15 @@
 //
 //  1. k_fuse_stats   z_i = (1 - alpha) o_i + alpha r_i (Eq. 2, fp32, no FMA
 //                    contraction, so alpha = 0 and alpha = 1 give o and r
-//                    exactly) and, per vocabulary chunk, the running max and
-//                    sum of exp for o, r and z plus z's top-2 and argmax.
-//  2. k_accept       per sequence: merges the chunks in index order, takes
-//                    x_hat_i = argmax z_i (lowest id on ties), accepts the
-//                    leading drafts equal to x_hat (Algorithm 2 at
-//                    temperature 0), emits t = x_hat_{n+1}, appends
+//                    exactly) and, per vocabulary chunk, the max, the sum of
+//                    exp and the centred sum of exp * (x - max) of o, r and
+//                    z, plus z's top-2 and argmax.
+//  2. k_accept       per sequence: merges the chunks in index order, gives
+//                    log-sum-exp and entropy (H = log S - S1 / S for the
+//                    centred sums), x_hat_i = argmax z_i (lowest id on
+//                    ties), applies the exact-match rule (Algorithm 2 at
+//                    temperature 0) or the entropy-thresholded rule
+//                    (Algorithm 3), emits t = x_hat_{n+1} and appends
 //                    x_1..x_n, t to the id history.
 //  3. k_logprob      log-softmax rows of o, r and z (pass two).
 #include "rv_internal.h"
@@ -32,24 +35,53 @@ RV_DEV Top top_merge(Top a, Top b) {
   return a;
 }
 
-RV_DEV void lse_merge(float& m, float& s, float m2, float s2) {
-  const float mn = fmaxf(m, m2);
-  if (mn == -INFINITY) return;
-  s = s * __expf(m - mn) + s2 * __expf(m2 - mn);
-  m = mn;
+// Softmax statistics of a set of values: max m, S = sum exp(x - m) and the
+// centred S1 = sum exp(x - m) (x - m).  Empty sets have m = -inf, S = S1 = 0.
+struct Stat {
+  float m, s, s1;
+};
+
+RV_DEV Stat stat_merge(Stat a, Stat b) {
+  const float mn = fmaxf(a.m, b.m);
+  if (mn == -INFINITY) return a;
+  Stat r{mn, 0.f, 0.f};
+  if (a.m != -INFINITY) {
+    const float d = a.m - mn, e = __expf(d);
+    r.s += a.s * e;
+    r.s1 += e * (a.s1 + a.s * d);
+  }
+  if (b.m != -INFINITY) {
+    const float d = b.m - mn, e = __expf(d);
+    r.s += b.s * e;
+    r.s1 += e * (b.s1 + b.s * d);
+  }
+  return r;
 }
 
-RV_DEV void lse_add(float& m, float& s, float x) {
-  if (x > m) {
-    s = s * __expf(m - x) + 1.0f;
-    m = x;
-  } else {
-    s += __expf(x - m);
-  }
+RV_DEV Stat stat_shfl(Stat a, int off) {
+  return Stat{__shfl_xor(a.m, off, 64), __shfl_xor(a.s, off, 64), __shfl_xor(a.s1, off, 64)};
+}
+
+template <int E>
+RV_DEV Stat stat_of(const float (&x)[E], int n_valid) {
+  float m = -INFINITY;
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+    if (e < n_valid) m = fmaxf(m, x[e]);
+  Stat r{m, 0.f, 0.f};
+  if (m == -INFINITY) return r;
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+    if (e < n_valid) {
+      const float d = x[e] - m, p = __expf(d);
+      r.s += p;
+      r.s1 += p * d;
+    }
+  return r;
 }
 
 // One workgroup per (vocabulary chunk of 2048, fused row); each thread owns 8
-// entries and loads them all before computing.
+// entries, strided by 256, and loads them all before computing.
 __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
   constexpr int E = 8;
   const int chunk = blockIdx.x, row = blockIdx.y;  // row = b*(k+1) + i
@@ -59,67 +91,75 @@ __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
   float* z = a.z + (size_t)row * a.V;
   const float wa = a.alpha, wo = 1.0f - a.alpha;
   const int v0 = chunk * a.chunk, v1 = min(a.V, v0 + a.chunk);
-  float ov[E], rv[E];
+  float ov[E], rv[E], zv[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const int v = min(v0 + threadIdx.x + e * 256, v1 - 1);
     ov[e] = o[v];
     rv[e] = r[v];
   }
-  float mo = -INFINITY, so = 0.f, mr = -INFINITY, sr = 0.f, mz = -INFINITY, sz = 0.f;
+  // entries e < n_valid are inside the chunk (v increases with e)
+  const int n_valid = min(E, max(0, (v1 - v0 - (int)threadIdx.x + 255) / 256));
   // start from a valid id, so the argmax stays in the vocabulary even if
   // no value compares greater (NaN logits)
   Top t{-INFINITY, v0, -INFINITY};
 #pragma unroll
   for (int e = 0; e < E; ++e) {
-    const int v = v0 + threadIdx.x + e * 256;
-    if (v >= v1) continue;
     const float zo = wo * ov[e];
     const float zr = wa * rv[e];
-    const float zv = zo + zr;
-    z[v] = zv;
-    lse_add(mo, so, ov[e]);
-    lse_add(mr, sr, rv[e]);
-    lse_add(mz, sz, zv);
-    if (zv > t.m1) {
-      t.m2 = t.m1;
-      t.m1 = zv;
-      t.i1 = v;
-    } else if (zv > t.m2) {
-      t.m2 = zv;
+    zv[e] = zo + zr;
+    if (e < n_valid) {
+      const int v = v0 + threadIdx.x + e * 256;
+      z[v] = zv[e];
+      if (zv[e] > t.m1) {
+        t.m2 = t.m1;
+        t.m1 = zv[e];
+        t.i1 = v;
+      } else if (zv[e] > t.m2) {
+        t.m2 = zv[e];
+      }
     }
   }
+  Stat so = stat_of(ov, n_valid), sr = stat_of(rv, n_valid), sz = stat_of(zv, n_valid);
   // wave reduction then LDS across the 4 waves
   for (int off = 32; off > 0; off >>= 1) {
-    lse_merge(mo, so, __shfl_xor(mo, off, 64), __shfl_xor(so, off, 64));
-    lse_merge(mr, sr, __shfl_xor(mr, off, 64), __shfl_xor(sr, off, 64));
-    lse_merge(mz, sz, __shfl_xor(mz, off, 64), __shfl_xor(sz, off, 64));
+    so = stat_merge(so, stat_shfl(so, off));
+    sr = stat_merge(sr, stat_shfl(sr, off));
+    sz = stat_merge(sz, stat_shfl(sz, off));
     Top u{__shfl_xor(t.m1, off, 64), __shfl_xor(t.i1, off, 64), __shfl_xor(t.m2, off, 64)};
     t = top_merge(t, u);
   }
-  __shared__ float sh[4][9];
+  __shared__ Stat sh_st[4][3];
+  __shared__ Top sh_top[4];
   const int w = threadIdx.x >> 6;
   if ((threadIdx.x & 63) == 0) {
-    sh[w][0] = mo; sh[w][1] = so; sh[w][2] = mr; sh[w][3] = sr; sh[w][4] = mz; sh[w][5] = sz;
-    sh[w][6] = t.m1; sh[w][7] = __int_as_float(t.i1); sh[w][8] = t.m2;
+    sh_st[w][0] = so;
+    sh_st[w][1] = sr;
+    sh_st[w][2] = sz;
+    sh_top[w] = t;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
     for (int ww = 1; ww < 4; ++ww) {
-      lse_merge(mo, so, sh[ww][0], sh[ww][1]);
-      lse_merge(mr, sr, sh[ww][2], sh[ww][3]);
-      lse_merge(mz, sz, sh[ww][4], sh[ww][5]);
-      t = top_merge(t, Top{sh[ww][6], __float_as_int(sh[ww][7]), sh[ww][8]});
+      so = stat_merge(so, sh_st[ww][0]);
+      sr = stat_merge(sr, sh_st[ww][1]);
+      sz = stat_merge(sz, sh_st[ww][2]);
+      t = top_merge(t, sh_top[ww]);
     }
     const int R1 = a.B * k1;
-    float* p0 = a.part + ((size_t)(0 * R1 + row) * a.nchunk + chunk) * 4;
-    float* p1 = a.part + ((size_t)(1 * R1 + row) * a.nchunk + chunk) * 4;
-    float* p2 = a.part + ((size_t)(2 * R1 + row) * a.nchunk + chunk) * 4;
-    p0[0] = mo; p0[1] = so;
-    p1[0] = mr; p1[1] = sr;
-    p2[0] = mz; p2[1] = sz; p2[2] = __int_as_float(t.i1); p2[3] = t.m1;
-    // second value is kept in the o slot's spare fields
-    p0[2] = t.m2;
+    const Stat st[3] = {so, sr, sz};
+    for (int f = 0; f < 3; ++f) {
+      float* p = a.part + ((size_t)(f * R1 + row) * a.nchunk + chunk) * 4;
+      p[0] = st[f].m;
+      p[1] = st[f].s;
+      p[2] = st[f].s1;
+      p[3] = 0.f;
+    }
+    float* p = a.part + ((size_t)(3 * R1 + row) * a.nchunk + chunk) * 4;
+    p[0] = __int_as_float(t.i1);
+    p[1] = t.m1;
+    p[2] = t.m2;
+    p[3] = 0.f;
   }
 }
 
@@ -131,26 +171,35 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
   const int k1 = a.k + 1, R1 = a.B * k1;
   __shared__ int xhat[RV_MAX_DRAFTS + 1];
   __shared__ float top2[RV_MAX_DRAFTS + 1];
+  __shared__ float lse_z[RV_MAX_DRAFTS + 1];
+  __shared__ float ent[2][RV_MAX_DRAFTS + 1];
   for (int i = w; i < k1; i += 4) {
     const int row = b * k1 + i;
-    float m[3] = {-INFINITY, -INFINITY, -INFINITY}, s[3] = {0.f, 0.f, 0.f};
+    Stat st[3] = {{-INFINITY, 0.f, 0.f}, {-INFINITY, 0.f, 0.f}, {-INFINITY, 0.f, 0.f}};
     Top t{-INFINITY, 0x7fffffff, -INFINITY};
     for (int c = lane; c < a.nchunk; c += 64) {
       for (int f = 0; f < 3; ++f) {
         const float* p = a.part + ((size_t)(f * R1 + row) * a.nchunk + c) * 4;
-        lse_merge(m[f], s[f], p[0], p[1]);
+        st[f] = stat_merge(st[f], Stat{p[0], p[1], p[2]});
       }
-      const float* pz = a.part + ((size_t)(2 * R1 + row) * a.nchunk + c) * 4;
-      const float* po = a.part + ((size_t)(0 * R1 + row) * a.nchunk + c) * 4;
-      t = top_merge(t, Top{pz[3], __float_as_int(pz[2]), po[2]});
+      const float* pt = a.part + ((size_t)(3 * R1 + row) * a.nchunk + c) * 4;
+      t = top_merge(t, Top{pt[1], __float_as_int(pt[0]), pt[2]});
     }
     for (int off = 32; off > 0; off >>= 1) {
-      for (int f = 0; f < 3; ++f) lse_merge(m[f], s[f], __shfl_xor(m[f], off, 64), __shfl_xor(s[f], off, 64));
+      for (int f = 0; f < 3; ++f) st[f] = stat_merge(st[f], stat_shfl(st[f], off));
       Top u{__shfl_xor(t.m1, off, 64), __shfl_xor(t.i1, off, 64), __shfl_xor(t.m2, off, 64)};
       t = top_merge(t, u);
     }
     if (lane == 0) {
-      for (int f = 0; f < 3; ++f) a.lse[f * R1 + row] = m[f] + logf(s[f]);
+      for (int f = 0; f < 3; ++f) a.lse[f * R1 + row] = st[f].m + logf(st[f].s);
+      // entropy of the softmax: log S - S1 / S in the centred form
+      const float hz = logf(st[2].s) - st[2].s1 / st[2].s;
+      const float ho = logf(st[0].s) - st[0].s1 / st[0].s;
+      a.entropy[row] = hz;
+      a.entropy[R1 + row] = ho;
+      ent[0][i] = hz;
+      ent[1][i] = ho;
+      lse_z[i] = st[2].m + logf(st[2].s);
       t.i1 = min(max(t.i1, 0), a.V - 1);  // every id used as an index below is in range
       xhat[i] = t.i1;
       top2[i] = t.m2;
@@ -161,6 +210,8 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
   if (threadIdx.x != 0) return;
   int bad = a.seq_bad[b];
   for (int j = 0; j < a.S; ++j) bad |= a.row_bad[b * a.S + j];
+  float* mg = a.margins + (size_t)b * (a.k + 2);
+  for (int i = 0; i < a.k + 2; ++i) mg[i] = NAN;
   if (bad) {
     a.accept_len[b] = -1;
     a.next_id[b] = -1;
@@ -168,10 +219,31 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
   }
   const int* x = a.drafts + (size_t)b * a.k;
   int n = a.k;
-  for (int i = 0; i < a.k; ++i) {
-    if (xhat[i] != x[i]) {
-      n = i;
-      break;
+  if (a.rule == RV_RULE_TYPICAL) {
+    // log p_i(x_i) > min(log eps, log delta - H_i)  (eps = inf, delta = 0 exact)
+    const float log_eps = logf(a.eps), log_delta = logf(a.delta);
+    const int src = a.ent_src == RV_ENTROPY_ORIGINAL ? 1 : 0;
+    for (int i = 0; i < a.k; ++i) {
+      const float lp = a.z[((size_t)b * k1 + i) * a.V + x[i]] - lse_z[i];
+      const float m = lp - fminf(log_eps, log_delta - ent[src][i]);
+      mg[i] = m;
+      if (!(m > 0.f)) {
+        n = i;
+        break;
+      }
+    }
+  } else {
+    for (int i = 0; i < a.k; ++i) {
+      if (xhat[i] != x[i]) {
+        n = i;
+        break;
+      }
+    }
+    // margins of the tested drafts (inspection only)
+    for (int i = 0; i < min(n + 1, a.k); ++i) {
+      const float* zi = a.z + ((size_t)b * k1 + i) * a.V;
+      const float zx = zi[x[i]];
+      mg[i] = xhat[i] == x[i] ? zx - top2[i] : zx - zi[xhat[i]];
     }
   }
   const int t = xhat[n];
@@ -181,15 +253,7 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
   int* hist = a.ids + (size_t)b * a.max_len;
   for (int i = 0; i < n; ++i) hist[L + i] = x[i];
   hist[L + n] = t;
-  // margins of the tested drafts and the bonus-token gap (inspection only)
-  float* mg = a.margins + (size_t)b * (a.k + 2);
-  for (int i = 0; i < a.k + 2; ++i) mg[i] = NAN;
-  for (int i = 0; i < min(n + 1, a.k); ++i) {
-    const float* zi = a.z + ((size_t)b * k1 + i) * a.V;
-    const float zx = zi[x[i]];
-    const float top = zi[xhat[i]];
-    mg[i] = xhat[i] == x[i] ? zx - top2[i] : zx - top;
-  }
+  // bonus-token gap
   mg[a.k + 1] = a.z[((size_t)b * k1 + n) * a.V + t] - top2[n];
 }
 

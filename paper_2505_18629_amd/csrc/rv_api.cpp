@@ -103,7 +103,7 @@ struct rv_cache {
   float *part_o, *part_ml;
   float* gpart;  // k-group partials of a split matmul [gk][rows][max(d_model, qkv rows)], gk*rows <= gpart_rows
   int gpart_rows;
-  float *logits, *z, *lp, *hpart, *lse, *margins;
+  float *logits, *z, *lp, *hpart, *lse, *margins, *entropy;
   int* argmax;
   int last_k = -1;
   // event profiler
@@ -223,9 +223,10 @@ size_t cache_layout(rv_cache* c, void* buf) {
   c->logits = cv.take<float*>((size_t)c->out_rows_cap * mc.vocab * 4);
   c->z = cv.take<float*>((size_t)c->r1_cap * mc.vocab * 4);
   c->lp = cv.take<float*>((size_t)3 * c->r1_cap * mc.vocab * 4);
-  c->hpart = cv.take<float*>((size_t)3 * c->r1_cap * c->nchunk * 4 * 4);
+  c->hpart = cv.take<float*>((size_t)4 * c->r1_cap * c->nchunk * 4 * 4);
   c->lse = cv.take<float*>((size_t)3 * c->r1_cap * 4);
   c->margins = cv.take<float*>((size_t)c->B * (c->max_drafts + 2) * 4);
+  c->entropy = cv.take<float*>((size_t)2 * c->r1_cap * 4);
   c->argmax = cv.take<int*>((size_t)c->r1_cap * 4);
   return align_up(cv.off, kAlign);
 }
@@ -761,7 +762,14 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   if (n_probe > 0 && !d_probe_ids) return fail(RV_E_ARG, "probe ids are NULL");
   if (!(fusion->alpha >= 0.f && fusion->alpha <= 1.f)) return fail(RV_E_ARG, "alpha must be in [0, 1]");
   if (fusion->prefix_pos < 0) return fail(RV_E_ARG, "prefix_pos must be >= 0");
-  if (fusion->rule != RV_RULE_GREEDY) return fail(RV_E_ARG, "unknown verification rule %d", fusion->rule);
+  if (fusion->rule != RV_RULE_GREEDY && fusion->rule != RV_RULE_TYPICAL)
+    return fail(RV_E_ARG, "unknown verification rule %d", fusion->rule);
+  if (fusion->rule == RV_RULE_TYPICAL) {
+    if (!(fusion->epsilon > 0.f)) return fail(RV_E_ARG, "epsilon must be > 0");
+    if (!(fusion->delta >= 0.f)) return fail(RV_E_ARG, "delta must be >= 0");
+    if (fusion->entropy_src != RV_ENTROPY_FUSED && fusion->entropy_src != RV_ENTROPY_ORIGINAL)
+      return fail(RV_E_ARG, "unknown entropy source %d", fusion->entropy_src);
+  }
   const int P = fusion->prefix_pos;
   const long long S = 1LL + 2LL * k + n_probe + P;
   if (S > c->max_block) return fail(RV_E_CAPACITY, "block of %lld rows exceeds max_block=%d", S, c->max_block);
@@ -845,6 +853,11 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   ha.nchunk = c->nchunk;
   ha.chunk = kVocabChunk;
   ha.alpha = fusion->alpha;
+  ha.rule = fusion->rule;
+  ha.eps = fusion->epsilon;
+  ha.delta = fusion->delta;
+  ha.ent_src = fusion->entropy_src;
+  ha.entropy = c->entropy;
   ha.logits = c->logits;
   ha.z = c->z;
   ha.part = c->hpart;
@@ -870,11 +883,19 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
 rv_status rv_debug_output(const rv_cache* c, int32_t which, float* d_dst, size_t dst_bytes, void* stream) {
   if (!c || !d_dst) return fail(RV_E_ARG, "cache and destination must not be NULL");
   if (c->last_k < 0) return fail(RV_E_STATE, "no verify has run on this cache");
-  if (which < RV_OUT_ORIG || which > RV_OUT_LOGP_FUSED) return fail(RV_E_ARG, "unknown output %d", which);
+  if (which < RV_OUT_ORIG || which > RV_OUT_MARGINS) return fail(RV_E_ARG, "unknown output %d", which);
   const int k1 = c->last_k + 1;
+  hipStream_t st = (hipStream_t)stream;
+  if (which == RV_OUT_ENTROPY || which == RV_OUT_MARGINS) {
+    const size_t n = which == RV_OUT_ENTROPY ? (size_t)2 * c->B * k1 : (size_t)c->B * (k1 + 1);
+    if (dst_bytes < n * 4) return fail(RV_E_BUFFER, "destination needs %zu bytes", n * 4);
+    HIP_TRY(hipMemcpyAsync(d_dst, which == RV_OUT_ENTROPY ? c->entropy : c->margins, n * 4,
+                           hipMemcpyDeviceToDevice, st),
+            "copy");
+    return RV_OK;
+  }
   const size_t V = c->m->cfg.vocab, row_bytes = (size_t)k1 * V * 4;
   if (dst_bytes < row_bytes * c->B) return fail(RV_E_BUFFER, "destination needs %zu bytes", row_bytes * c->B);
-  hipStream_t st = (hipStream_t)stream;
   if (which == RV_OUT_ORIG || which == RV_OUT_REFL) {
     const float* src = c->logits + (which == RV_OUT_REFL ? (size_t)k1 * V : 0);
     HIP_TRY(hipMemcpy2DAsync(d_dst, row_bytes, src, 2 * row_bytes, row_bytes, c->B, hipMemcpyDeviceToDevice, st),

@@ -170,10 +170,14 @@ hipError_t launch_store_ids(const StoreIds& s, hipStream_t st);
 struct HeadArgs {
   int B, k, V, S, max_len, nchunk, chunk;
   float alpha;
+  int rule;              // RV_RULE_GREEDY / RV_RULE_TYPICAL
+  float eps, delta;      // typical threshold parameters
+  int ent_src;           // RV_ENTROPY_FUSED / RV_ENTROPY_ORIGINAL
   const float* logits;   // [B][2(k+1)][V]: o rows then r rows per sequence
   float* z;              // [B][k+1][V]
-  float* part;           // [3 * B*(k+1)][nchunk][4]
+  float* part;           // [4][B*(k+1)][nchunk][4]: (max, sum, centred sum) of o, r, z; z's top-2
   float* lse;            // [3][B*(k+1)]
+  float* entropy;        // [2][B*(k+1)]: entropy of softmax(z), then of softmax(o)
   float* lp;             // [3][B][k+1][V]: log-softmax of o, r, z
   float* margins;        // [B][k+2]: margins of tested drafts, then top1-top2 gap
   const int* drafts;     // [B][k]

@@ -204,3 +204,35 @@ def test_full_8b_commit_matches_fresh_prefill(rv, gpu, model8b, verify8b):
             # differences that grow slowly through the layers
             assert np.abs(a_ - b_).max() <= 1e-3 * np.abs(b_).max(), (layer, float(np.abs(a_ - b_).max()))
     fresh.close()
+
+
+def test_full_8b_typical_rule_properties(rv, model8b, verify8b):
+    """Algorithm 3's rule at the full 8B shape: the decision equals the rule
+    applied to the GPU's own log-probabilities and entropies; eps = inf with
+    delta = 0 accepts every draft."""
+    import torch
+    d = verify8b
+    w = d["w"]
+    drafts = list(workload.corrupt(d["greedy"][:w.k], 0.5, SHAPE.vocab, np.random.default_rng(9)))
+    for eps, delta, src in ((0.09, 0.3, rv.RV_ENTROPY_FUSED), (0.5, 2.0, rv.RV_ENTROPY_ORIGINAL)):
+        acc, nxt = model8b.verify(d["lens"], np.array([drafts]), d["probe"], w.alpha, w.prefix_pos,
+                                  rule=rv.RV_RULE_TYPICAL, epsilon=eps, delta=delta, entropy_src=src)
+        torch.cuda.synchronize()
+        n, t = int(acc[0]), int(nxt[0])
+        lp = model8b.output(rv.RV_OUT_LOGP_FUSED).cpu().numpy()[0].astype(np.float64)
+        z = model8b.output(rv.RV_OUT_FUSED).cpu().numpy()[0]
+        H = model8b.output(rv.RV_OUT_ENTROPY).cpu().numpy()[:, 0].astype(np.float64)
+        h = H[0] if src == rv.RV_ENTROPY_FUSED else H[1]
+        # the entropies are those of the GPU's own log-probabilities
+        lpo = model8b.output(rv.RV_OUT_LOGP_ORIG).cpu().numpy()[0].astype(np.float64)
+        np.testing.assert_allclose(H[0], -(np.exp(lp) * lp).sum(-1), atol=2e-3)
+        np.testing.assert_allclose(H[1], -(np.exp(lpo) * lpo).sum(-1), atol=2e-3)
+        margins = [lp[i][drafts[i]] - min(np.log(eps), np.log(delta) - h[i]) for i in range(w.k)]
+        n_ref = next((i for i, m in enumerate(margins) if not m > 0), w.k)
+        if all(abs(m) > 1e-3 for m in margins[:n_ref + 1]):
+            assert (n, t) == (n_ref, int(np.argmax(z[n_ref])))
+    acc, nxt = model8b.verify(d["lens"], np.array([drafts]), d["probe"], w.alpha, w.prefix_pos,
+                              rule=rv.RV_RULE_TYPICAL, epsilon=float("inf"), delta=0.0)
+    torch.cuda.synchronize()
+    z = model8b.output(rv.RV_OUT_FUSED).cpu().numpy()[0]
+    assert (int(acc[0]), int(nxt[0])) == (w.k, int(np.argmax(z[w.k])))

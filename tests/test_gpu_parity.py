@@ -30,8 +30,10 @@ def logits_close(shape, got, ref):
 class Case:
     """Prefill + one verify on the GPU; the oracle recomputes each sequence."""
 
-    def __init__(self, rv, shape, seed, histories, drafts, probe, alpha, P, max_len=None):
+    def __init__(self, rv, shape, seed, histories, drafts, probe, alpha, P, max_len=None, typical=None):
+        """typical: None (Algorithm 2) or (epsilon, delta, entropy_of) for Algorithm 3."""
         import torch
+        self.typical = typical
         self.shape, self.seed = shape, seed
         self.histories = [list(map(int, h)) for h in histories]
         self.drafts = np.asarray(drafts, dtype=np.int32).reshape(len(histories), -1)
@@ -43,15 +45,24 @@ class Case:
         max_len = max_len or (max(len(h) for h in histories) + S + 8)
         self.v = rv.Verifier(shape, seed, B, max_len, max_block=max(S, 8), max_drafts=max(k, 1))
         self.lens = self.v.prefill(self.histories)
-        acc, nxt = self.v.verify(self.lens, self.drafts, self.probe, alpha, P)
+        kw = {}
+        if typical:
+            eps, delta, src = typical
+            kw = dict(rule=rv.RV_RULE_TYPICAL, epsilon=eps, delta=delta,
+                      entropy_src=rv.RV_ENTROPY_FUSED if src == "fused" else rv.RV_ENTROPY_ORIGINAL)
+        acc, nxt = self.v.verify(self.lens, self.drafts, self.probe, alpha, P, **kw)
         torch.cuda.synchronize()
         self.accept_len = acc.cpu().numpy().copy()
         self.next_id = nxt.cpu().numpy().copy()
-        self.out = {w: self.v.output(w).cpu().numpy() for w in range(6)}
+        self.out = {w: self.v.output(w).cpu().numpy() for w in range(8)}
 
     def oracle(self, b):
+        kw = {}
+        if self.typical:
+            eps, delta, src = self.typical
+            kw = dict(rule="typical", eps=eps, delta=delta, entropy_of=src)
         return oracle.verify(self.shape, self.seed, self.histories[b], self.drafts[b], self.probe,
-                             self.alpha, self.P)
+                             self.alpha, self.P, **kw)
 
     def check(self, rv):
         for b in range(len(self.histories)):
@@ -65,9 +76,18 @@ class Case:
             lp_ref = ref["lp_z"]
             assert np.abs(self.out[rv.RV_OUT_LOGP_FUSED][b] - lp_ref).max() < (
                 1e-4 if self.shape.dtype == "f32" else 0.05 * np.abs(lp_ref).max())
+            # entropies of the fused and original rows
+            h_tol = 5e-4 if self.shape.dtype == "f32" else 2e-2 * max(1.0, float(np.abs(ref["h_z"]).max()))
+            assert np.abs(self.out[rv.RV_OUT_ENTROPY][0][b] - ref["h_z"]).max() < h_tol
+            assert np.abs(self.out[rv.RV_OUT_ENTROPY][1][b] - ref["h_o"]).max() < h_tol
             if not ref["near_tie"]:
                 assert (int(self.accept_len[b]), int(self.next_id[b])) == (ref["accept_len"], ref["next_id"]), (
                     b, ref["margins"], ref["gap"])
+                mg = self.out[rv.RV_OUT_MARGINS][b]
+                n_tested = len(ref["margins"])
+                m_tol = 1e-3 if self.shape.dtype == "f32" else 5e-2
+                np.testing.assert_allclose(mg[:n_tested], ref["margins"], atol=m_tol)
+                assert np.isnan(mg[n_tested:-1]).all()
         return True
 
 
@@ -127,6 +147,21 @@ def test_tiny_bf16_gqa_matches_oracle(rv, gpu, alpha, P, n_probe, k):
     probe = workload.random_ids(shape.vocab, n_probe, 2, 0xBEEF)
     c = Case(rv, shape, 1, hists, drafts, probe, alpha, P)
     c.check(rv)
+    c.v.close()
+
+
+@pytest.mark.parametrize("shape", [workload.TINY, workload.TINY_GQA_BF16], ids=lambda s: s.name)
+@pytest.mark.parametrize("alpha,typical", [(0.3, (0.09, 0.3, "fused")), (1.0, (0.3, 0.1, "original")),
+                                           (0.3, (float("inf"), 0.0, "fused")), (0.0, (0.05, 2.0, "fused"))])
+def test_typical_rule_matches_oracle(rv, gpu, shape, alpha, typical):
+    """Algorithm 3's entropy-thresholded rule against the oracle."""
+    hists = [workload.random_ids(shape.vocab, L, 5, b) for b, L in enumerate([60, 97])]
+    drafts = [draft_case(shape, 3, h, 5, 0.5, 50 + b) for b, h in enumerate(hists)]
+    probe = workload.random_ids(shape.vocab, 6, 5, 0xBEEF)
+    c = Case(rv, shape, 3, hists, drafts, probe, alpha, 4, typical=typical)
+    c.check(rv)
+    if typical[0] == float("inf") and typical[1] == 0.0:
+        assert (c.accept_len == 5).all()
     c.v.close()
 
 
@@ -220,6 +255,11 @@ def test_validation_errors_enqueue_nothing(rv, gpu):
     assert code(k=5) == "RV_E_ARG"
     assert code(prefix_pos=-1) == "RV_E_ARG"
     assert code(rule=3) == "RV_E_ARG"
+    typ = dict(rule=rv.RV_RULE_TYPICAL)
+    assert code(epsilon=0.0, **typ) == "RV_E_ARG"
+    assert code(epsilon=float("nan"), **typ) == "RV_E_ARG"
+    assert code(delta=-0.1, **typ) == "RV_E_ARG"
+    assert code(entropy_src=2, **typ) == "RV_E_ARG"
     assert code(prefix_len=[1], prefix_pos=2) == "RV_E_RANGE"
     assert code(prefix_len=[41]) == "RV_E_RANGE"
     assert code(prefix_len=[35]) == "RV_E_CAPACITY"
