@@ -14,6 +14,10 @@ What it computes (arXiv 2505.18629):
   * Appendix A, Algorithm 2 (exact-match verification), at temperature 0.
   * Appendix A, Algorithm 3 (entropy-thresholded "typical" acceptance) with
     a greedy bonus token.
+  * Algorithm 1 (speculative sampling): uniform acceptance tests against
+    p_i / q_i and a draw from norm(max(0, p - q)), with the random numbers
+    taken from Philox4x64-10 (Salmon et al., SC 2011) under a fixed counter
+    layout, so that the GPU library can draw the same ones.
 
 Because one causal pass produces exactly the next-token logits at every block
 position, the oracle is that definition written out: a plain Llama-style
@@ -397,11 +401,100 @@ def accept_typical(z: np.ndarray, o: np.ndarray, drafts: Sequence[int], eps: flo
     return n, t, margins
 
 
+# ------------------------------------------------------------ randomness
+# Philox4x64-10: a 10-round counter-based generator; each round multiplies
+# counter words 0 and 2 by fixed odd constants (full 128-bit products), mixes
+# the high halves with the other words and the key, and the key is advanced by
+# two Weyl constants between rounds.
+_PHILOX_M = (0xD2E7470EE14C6C93, 0xCA5A826395121157)
+_PHILOX_W = (0x9E3779B97F4A7C15, 0xBB67AE8584CAA73B)
+_M64 = (1 << 64) - 1
+
+
+def philox4x64(counter: Sequence[int], key: Sequence[int]) -> List[int]:
+    c = [int(x) & _M64 for x in counter]
+    k0, k1 = int(key[0]) & _M64, int(key[1]) & _M64
+    for rnd in range(10):
+        p0, p1 = _PHILOX_M[0] * c[0], _PHILOX_M[1] * c[2]
+        c = [((p1 >> 64) ^ c[1] ^ k0) & _M64, p1 & _M64, ((p0 >> 64) ^ c[3] ^ k1) & _M64, p0 & _M64]
+        if rnd < 9:
+            k0, k1 = (k0 + _PHILOX_W[0]) & _M64, (k1 + _PHILOX_W[1]) & _M64
+    return c
+
+
+def uniform24(word: int) -> float:
+    """The top 23 bits of a 64-bit word as a uniform in (0, 1): (w >> 41) + 1/2
+    over 2^23, whose odd 24-bit numerator makes it exact in fp32 and fp64."""
+    return ((int(word) >> 41) + 0.5) / float(1 << 23)
+
+
+def acceptance_uniform(seed: int, seq: int, i: int) -> float:
+    """r_i of sequence slot `seq` (Algorithm 1): word 0 of Philox at counter
+    (i, seq, 0, 0), key (seed, 0)."""
+    return uniform24(philox4x64((i, seq, 0, 0), (seed, 0))[0])
+
+
+def gumbel_uniforms(seed: int, seq: int, V: int) -> np.ndarray:
+    """One uniform per vocabulary id v for the bonus-token draw: word v % 4 of
+    Philox at counter (v // 4, seq, 1, 0), key (seed, 0)."""
+    u = np.empty(V, dtype=np.float64)
+    for blk in range((V + 3) // 4):
+        words = philox4x64((blk, seq, 1, 0), (seed, 0))
+        for j in range(4):
+            if 4 * blk + j < V:
+                u[4 * blk + j] = uniform24(words[j])
+    return u
+
+
+def accept_sampling(z: np.ndarray, q: np.ndarray, drafts: Sequence[int], seed: int, seq: int,
+                    tie_eps: float = 1e-3):
+    """Algorithm 1's speculative-sampling rule on the fused distribution
+    p_i = softmax(z_i) (z already divided by the temperature).
+
+    Draft i is rejected when r_i > p_i(x_i) / q_i(x_i), compared as
+    r_i * q_i(x_i) > p_i(x_i); n = leading accepted drafts.  The bonus token
+    is drawn from norm(max(0, p_{n+1} - q_{n+1})) if n < k, else from
+    p_{k+1}, as argmax_v (log w_v + G_v) with w the unnormalised weights and
+    G_v = -log(-log(u_v)) Gumbel noise (the Gumbel-max form of a categorical
+    draw; normalisation does not change the argmax).  Returns n, t, the
+    log-domain acceptance margins log p - log(r q) of the tested drafts,
+    the top-1 minus top-2 gap of the perturbed scores, and a near-tie flag."""
+    k = len(drafts)
+    lp = log_softmax(z)
+    n, margins = k, []
+    for i in range(k):
+        x = int(drafts[i])
+        r = acceptance_uniform(seed, seq, i)
+        p_x, q_x = float(np.exp(lp[i][x])), float(q[i][x])
+        m = np.inf if q_x <= 0 else float(np.log(p_x) - np.log(r * q_x))
+        margins.append(m)
+        if r * q_x > p_x:
+            n = i
+            break
+    if n < k:
+        w = np.exp(lp[n]) - np.asarray(q[n], dtype=np.float64)
+        with np.errstate(divide="ignore"):
+            score = np.where(w > 0, np.log(np.maximum(w, 1e-300)), -np.inf)
+    else:
+        score = lp[k]
+    u = gumbel_uniforms(seed, seq, z.shape[-1])
+    s = score - np.log(-np.log(u))
+    t = int(np.argmax(s))
+    top = np.sort(s)[-2:]
+    gap = float(top[1] - top[0])
+    near = any(abs(m) < tie_eps for m in margins) or gap < tie_eps
+    return n, t, margins, gap, near
+
+
 def verify(shape, seed: int, history: Sequence[int], drafts: Sequence[int], probe: Sequence[int],
            alpha: float, prefix_pos: int, mode: str = "contract", rule: str = "greedy", eps: float = 0.09,
-           delta: float = 0.3, entropy_of: str = "fused", tie_eps: float = 1e-3) -> Dict:
+           delta: float = 0.3, entropy_of: str = "fused", tie_eps: float = 1e-3, temperature: float = 1.0,
+           q: np.ndarray | None = None, rng_seed: int = 0, seq: int = 0) -> Dict:
     """One verify step for one sequence: Algorithm 1's block with Algorithm
-    2's rule (rule="greedy") or Algorithm 3's (rule="typical")."""
+    2's rule (rule="greedy"), Algorithm 3's (rule="typical") or Algorithm 1's
+    speculative sampling (rule="sampling", draft distributions q [k][V],
+    random numbers from (rng_seed, seq)).  The fused logits are divided by
+    the temperature (fp32) before any rule."""
     history = [int(t) for t in history]
     drafts = [int(t) for t in drafts]
     block, shift, orig_rows, refl_rows = reflective_block(history, drafts, probe, prefix_pos)
@@ -412,7 +505,11 @@ def verify(shape, seed: int, history: Sequence[int], drafts: Sequence[int], prob
     k = len(drafts)
     o, r = logits[: k + 1], logits[k + 1:]
     z = fuse(o, r, alpha)
-    if rule == "greedy":
+    if temperature != 1.0:
+        z = (z.astype(np.float32) / np.float32(temperature)).astype(np.float32)
+    if rule == "sampling":
+        n, t, ms, gap, near = accept_sampling(z.astype(np.float64), q, drafts, rng_seed, seq, tie_eps)
+    elif rule == "greedy":
         n, t = accept_greedy(z, drafts)
         ms, gap, near = decision_margins(z, drafts, n, tie_eps)
     elif rule == "typical":

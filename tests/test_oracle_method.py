@@ -186,3 +186,89 @@ def test_typical_monotone_and_end_points():
         for d in (0.1, 0.4):
             assert oracle.accept_typical(z0, o, drafts, 0.3, d, "fused") == \
                 oracle.accept_typical(z0, o, drafts, 0.3, d, "original")
+
+
+# ------------------------------------------------------------ Algorithm 1 (sampling)
+
+def test_philox_matches_numpy_stream():
+    """numpy's Philox bit generator is Philox4x64-10; it advances the counter
+    before each block, so its first block is counter + 1."""
+    for key, ctr in (((123, 456), (0, 0, 0, 0)), ((2**64 - 1, 7), (2**64 - 1, 5, 0, 9)), ((0, 0), (3, 1, 4, 1))):
+        bg = np.random.Philox(key=np.array(key, dtype=np.uint64), counter=np.array(ctr, dtype=np.uint64))
+        raw = [int(x) for x in bg.random_raw(12)]
+        c = list(ctr)
+        mine = []
+        for _ in range(3):
+            # 256-bit little-endian increment
+            for j in range(4):
+                c[j] = (c[j] + 1) & (2**64 - 1)
+                if c[j]:
+                    break
+            mine += oracle.philox4x64(c, key)
+        assert mine == raw
+
+
+def test_uniform24_range_and_moments():
+    u = np.array([oracle.acceptance_uniform(5, s, i) for s in range(50) for i in range(200)])
+    assert (u > 0).all() and (u < 1).all()
+    assert np.array_equal(u.astype(np.float32).astype(np.float64), u)  # exact in fp32
+    assert abs(u.mean() - 0.5) < 0.01 and abs(u.var() - 1 / 12) < 0.005
+    g = oracle.gumbel_uniforms(9, 0, 4099)
+    assert g.shape == (4099,) and (g > 0).all() and (g < 1).all() and len(np.unique(g)) > 4000
+
+
+def test_sampling_p_equals_q_accepts_everything():
+    rng = np.random.default_rng(4)
+    for seed in range(20):
+        z = (rng.standard_normal((4, 9)) * 2).astype(np.float32).astype(np.float64)
+        q = np.exp(oracle.log_softmax(z))
+        drafts = [int(rng.choice(9, p=q[i] / q[i].sum())) for i in range(3)]
+        n, t, margins, gap, near = oracle.accept_sampling(z, q[:3], drafts, seed, 0)
+        assert n == 3 and all(m >= 0 for m in margins)
+
+
+def _first_token_counts(z, q, trials, sample_bonus_from_p=False):
+    """Emitted first token over many (seed, drafts): x_1 if accepted, else t."""
+    rng = np.random.default_rng(12)
+    V = z.shape[-1]
+    counts = np.zeros(V)
+    for seed in range(trials):
+        drafts = [int(rng.choice(V, p=q[i])) for i in range(q.shape[0])]
+        if sample_bonus_from_p:
+            # planted mistake: the rejected position re-draws from p, not from the residual
+            n, _, _, _, _ = oracle.accept_sampling(z, q, drafts, seed, 1)
+            tok = drafts[0] if n >= 1 else int(rng.choice(V, p=np.exp(oracle.log_softmax(z[0]))))
+        else:
+            n, t, _, _, _ = oracle.accept_sampling(z, q, drafts, seed, 1)
+            tok = drafts[0] if n >= 1 else t
+        counts[tok] += 1
+    return counts
+
+
+def test_sampling_first_token_follows_p():
+    """Speculative sampling is exact: the first emitted token is distributed
+    as p_1 whatever the draft distribution (chi-square test)."""
+    rng = np.random.default_rng(21)
+    V, k, trials = 6, 2, 6000
+    z = (rng.standard_normal((k + 1, V)) * 1.5).astype(np.float32).astype(np.float64)
+    ql = rng.standard_normal((k, V)) * 1.5
+    q = np.exp(ql - scipy.special.logsumexp(ql, axis=-1, keepdims=True))
+    p1 = np.exp(oracle.log_softmax(z[0]))
+    counts = _first_token_counts(z, q, trials)
+    assert scipy.stats.chisquare(counts, p1 * trials).pvalue > 1e-3
+    # the test has the power to see a wrong residual draw
+    bad = _first_token_counts(z, q, trials, sample_bonus_from_p=True)
+    assert scipy.stats.chisquare(bad, p1 * trials).pvalue < 1e-6
+
+
+def test_sampling_bonus_draw_follows_p_when_all_accepted():
+    """With no drafts the bonus token is a Gumbel-max draw from p_1."""
+    rng = np.random.default_rng(8)
+    V, trials = 5, 8000
+    z = (rng.standard_normal((1, V)) * 1.2).astype(np.float32).astype(np.float64)
+    counts = np.zeros(V)
+    for seed in range(trials):
+        _, t, _, _, _ = oracle.accept_sampling(z, np.zeros((0, V)), [], seed, 3)
+        counts[t] += 1
+    p = np.exp(oracle.log_softmax(z[0]))
+    assert scipy.stats.chisquare(counts, p * trials).pvalue > 1e-3
