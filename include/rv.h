@@ -52,7 +52,7 @@ typedef enum {
 } rv_status;
 
 enum { RV_F32 = 0, RV_BF16 = 1 };
-enum { RV_RULE_GREEDY = 0, RV_RULE_TYPICAL = 1 };
+enum { RV_RULE_GREEDY = 0, RV_RULE_TYPICAL = 1, RV_RULE_SAMPLING = 2 };
 enum { RV_ENTROPY_FUSED = 0, RV_ENTROPY_ORIGINAL = 1 };
 enum { RV_MAX_BATCH = 256, RV_MAX_DRAFTS = 32 };
 
@@ -83,14 +83,18 @@ typedef struct {
  *   entropy (nats) of p_i (RV_ENTROPY_FUSED) or of softmax(o_i)
  *   (RV_ENTROPY_ORIGINAL); compared in the log domain, so epsilon = +inf and
  *   delta = 0 are exact.
- * Both: n = leading accepted drafts, t = argmax z_{n+1} (lowest id on ties). */
+ * Both: n = leading accepted drafts, t = argmax z_{n+1} (lowest id on ties).
+ * RV_RULE_SAMPLING (Algorithm 1, rv_verify_sampled only): see there.
+ * z_i is the fused logit row divided by `temperature` (Table 5); greedy
+ * decisions do not depend on it. */
 typedef struct {
   float alpha;         /* weight of the reflective logits, 0 <= alpha <= 1 (Eq. 2) */
   int32_t prefix_pos;  /* P: committed tokens re-presented after the probe (Eq. 1) */
-  int32_t rule;        /* RV_RULE_GREEDY or RV_RULE_TYPICAL */
+  int32_t rule;        /* RV_RULE_GREEDY, RV_RULE_TYPICAL or RV_RULE_SAMPLING */
   float epsilon;       /* typical: threshold cap, > 0 (may be +inf) */
   float delta;         /* typical: entropy-scaled threshold factor, >= 0 */
   int32_t entropy_src; /* typical: RV_ENTROPY_FUSED or RV_ENTROPY_ORIGINAL */
+  float temperature;   /* > 0, finite; 1 leaves the fused logits unchanged */
 } rv_fusion;
 
 typedef struct rv_model rv_model;
@@ -163,6 +167,26 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
                     const int32_t* d_probe_ids, int32_t n_probe, const rv_fusion* fusion,
                     int32_t* d_accept_len, int32_t* d_next_id, void* stream);
 
+/* rv_verify with Algorithm 1's speculative-sampling rule (fusion->rule must
+ * be RV_RULE_SAMPLING).
+ *   d_draft_probs [batch][k][vocab] device fp32: the draft distributions q_i
+ *                 the drafts were sampled from (rows sum to 1; not checked).
+ *                 May be NULL when k == 0.
+ *   seed          key of the random numbers; a call is a pure function of
+ *                 its inputs and seed, so callers vary the seed per step.
+ * With p_i = softmax(z_i): draft i is rejected when r_i * q_i(x_i) >
+ * p_i(x_i) (r_i uniform); n = leading accepted drafts; t is drawn from
+ * norm(max(0, p_{n+1} - q_{n+1})) if n < k, else from p_{k+1}, as
+ * argmax_v (log w_v - log(-log u_v)) (Gumbel-max).  Random numbers:
+ * Philox4x64-10 (Salmon et al., SC 2011) with key (seed, 0); r_i is word 0
+ * at counter (i, b, 0, 0) and u_v word v % 4 at counter (v / 4, b, 1, 0),
+ * b the batch slot; a 64-bit word w becomes ((w >> 41) + 1/2) / 2^23.
+ * Everything else as rv_verify. */
+rv_status rv_verify_sampled(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t k,
+                            const float* d_draft_probs, const int32_t* d_probe_ids, int32_t n_probe,
+                            const rv_fusion* fusion, uint64_t seed, int32_t* d_accept_len,
+                            int32_t* d_next_id, void* stream);
+
 /* ---- inspection (tests and benchmarks) ---- */
 
 /* Which result of the last rv_verify to copy.  RV_OUT_ORIG .. RV_OUT_LOGP_FUSED
@@ -171,8 +195,9 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
  * [2][batch][k+1]: the entropy (nats) of softmax(z_i), then of softmax(o_i).
  * RV_OUT_MARGINS is fp32 [batch][k+2]: for each tested draft the distance of
  * its decision from the boundary (greedy: z_i[x_i] - max_{v != x_i} z_i[v];
- * typical: log p_i(x_i) - log threshold_i; NaN for untested drafts), then
- * NaN, then the top-1 minus top-2 gap of z_{n+1}. */
+ * typical: log p_i(x_i) - log threshold_i; sampling: log p_i(x_i) -
+ * log(r_i q_i(x_i)); NaN for untested drafts), then NaN, then the top-1
+ * minus top-2 gap of z_{n+1} (sampling: of the perturbed draw scores). */
 enum {
   RV_OUT_ORIG = 0, RV_OUT_REFL = 1, RV_OUT_FUSED = 2,
   RV_OUT_LOGP_ORIG = 3, RV_OUT_LOGP_REFL = 4, RV_OUT_LOGP_FUSED = 5,

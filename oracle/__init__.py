@@ -489,11 +489,11 @@ def accept_sampling(z: np.ndarray, q: np.ndarray, drafts: Sequence[int], seed: i
 def verify(shape, seed: int, history: Sequence[int], drafts: Sequence[int], probe: Sequence[int],
            alpha: float, prefix_pos: int, mode: str = "contract", rule: str = "greedy", eps: float = 0.09,
            delta: float = 0.3, entropy_of: str = "fused", tie_eps: float = 1e-3, temperature: float = 1.0,
-           q: np.ndarray | None = None, rng_seed: int = 0, seq: int = 0) -> Dict:
+           q: np.ndarray | None = None, rng_seed: int = 0, slot: int = 0) -> Dict:
     """One verify step for one sequence: Algorithm 1's block with Algorithm
     2's rule (rule="greedy"), Algorithm 3's (rule="typical") or Algorithm 1's
     speculative sampling (rule="sampling", draft distributions q [k][V],
-    random numbers from (rng_seed, seq)).  The fused logits are divided by
+    random numbers from (rng_seed, batch slot `slot`)).  The fused logits are divided by
     the temperature (fp32) before any rule."""
     history = [int(t) for t in history]
     drafts = [int(t) for t in drafts]
@@ -508,7 +508,7 @@ def verify(shape, seed: int, history: Sequence[int], drafts: Sequence[int], prob
     if temperature != 1.0:
         z = (z.astype(np.float32) / np.float32(temperature)).astype(np.float32)
     if rule == "sampling":
-        n, t, ms, gap, near = accept_sampling(z.astype(np.float64), q, drafts, rng_seed, seq, tie_eps)
+        n, t, ms, gap, near = accept_sampling(z.astype(np.float64), q, drafts, rng_seed, slot, tie_eps)
     elif rule == "greedy":
         n, t = accept_greedy(z, drafts)
         ms, gap, near = decision_margins(z, drafts, n, tie_eps)

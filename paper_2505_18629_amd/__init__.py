@@ -28,7 +28,7 @@ import torch  # noqa: E402,F401
 _lib = ctypes.CDLL(LIB_PATH)
 
 RV_F32, RV_BF16 = 0, 1
-RV_RULE_GREEDY, RV_RULE_TYPICAL = 0, 1
+RV_RULE_GREEDY, RV_RULE_TYPICAL, RV_RULE_SAMPLING = 0, 1, 2
 RV_ENTROPY_FUSED, RV_ENTROPY_ORIGINAL = 0, 1
 RV_MAX_BATCH, RV_MAX_DRAFTS = 256, 32
 (RV_OUT_ORIG, RV_OUT_REFL, RV_OUT_FUSED, RV_OUT_LOGP_ORIG, RV_OUT_LOGP_REFL, RV_OUT_LOGP_FUSED, RV_OUT_ENTROPY,
@@ -41,7 +41,7 @@ STATUS = {0: "RV_OK", -1: "RV_E_ARG", -2: "RV_E_RANGE", -3: "RV_E_CAPACITY", -4:
 
 EXPORTED = [
     "rv_status_str", "rv_last_error", "rv_model_bytes", "rv_init_weights", "rv_model_free",
-    "rv_cache_bytes", "rv_cache_create", "rv_cache_free", "rv_prefill_cache", "rv_verify",
+    "rv_cache_bytes", "rv_cache_create", "rv_cache_free", "rv_prefill_cache", "rv_verify", "rv_verify_sampled",
     "rv_debug_output", "rv_debug_export_kv", "rv_debug_export_ids", "rv_debug_weight_bits",
     "rv_debug_linear", "rv_debug_workspace", "rv_debug_profile", "rv_debug_profile_read", "rv_debug_time_matrix",
 ]
@@ -56,7 +56,8 @@ class rv_config(ctypes.Structure):
 
 class rv_fusion(ctypes.Structure):
     _fields_ = [("alpha", ctypes.c_float), ("prefix_pos", ctypes.c_int32), ("rule", ctypes.c_int32),
-                ("epsilon", ctypes.c_float), ("delta", ctypes.c_float), ("entropy_src", ctypes.c_int32)]
+                ("epsilon", ctypes.c_float), ("delta", ctypes.c_float), ("entropy_src", ctypes.c_int32),
+                ("temperature", ctypes.c_float)]
 
 
 class RVError(RuntimeError):
@@ -79,6 +80,8 @@ _sig = {
     "rv_cache_free": ([_vp], None),
     "rv_prefill_cache": ([_vp, _vp, _i32, _P_i32, _vp], ctypes.c_int),
     "rv_verify": ([_vp, _P_i32, _vp, _i32, _vp, _i32, ctypes.POINTER(rv_fusion), _vp, _vp, _vp], ctypes.c_int),
+    "rv_verify_sampled": ([_vp, _P_i32, _vp, _i32, _vp, _vp, _i32, ctypes.POINTER(rv_fusion), ctypes.c_uint64, _vp,
+                           _vp, _vp], ctypes.c_int),
     "rv_debug_output": ([_vp, _i32, _vp, _sz, _vp], ctypes.c_int),
     "rv_debug_export_kv": ([_vp, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp], ctypes.c_int),
     "rv_debug_export_ids": ([_vp, _i32, _i32, _i32, _vp, _vp], ctypes.c_int),
@@ -180,11 +183,21 @@ def rv_prefill_cache(cache: int, prefix_ids, prefix_len: Sequence[int], stream=N
 
 def rv_verify(cache: int, prefix_len: Sequence[int], draft_ids, k: int, probe_ids, n_probe: int, alpha: float,
               prefix_pos: int, accept_len, next_id, rule: int = RV_RULE_GREEDY, stream=None,
-              epsilon: float = 0.09, delta: float = 0.3, entropy_src: int = RV_ENTROPY_FUSED) -> None:
+              epsilon: float = 0.09, delta: float = 0.3, entropy_src: int = RV_ENTROPY_FUSED,
+              temperature: float = 1.0) -> None:
     _keep, lens = _host_i32(prefix_len)
-    fu = rv_fusion(alpha, prefix_pos, rule, epsilon, delta, entropy_src)
+    fu = rv_fusion(alpha, prefix_pos, rule, epsilon, delta, entropy_src, temperature)
     _check(_lib.rv_verify(cache, lens, _dev(draft_ids), k, _dev(probe_ids), n_probe, ctypes.byref(fu),
                           _dev(accept_len), _dev(next_id), _stream(stream)))
+
+
+def rv_verify_sampled(cache: int, prefix_len: Sequence[int], draft_ids, k: int, draft_probs, probe_ids,
+                      n_probe: int, alpha: float, prefix_pos: int, seed: int, accept_len, next_id,
+                      temperature: float = 1.0, rule: int = RV_RULE_SAMPLING, stream=None) -> None:
+    _keep, lens = _host_i32(prefix_len)
+    fu = rv_fusion(alpha, prefix_pos, rule, 0.0, 0.0, RV_ENTROPY_FUSED, temperature)
+    _check(_lib.rv_verify_sampled(cache, lens, _dev(draft_ids), k, _dev(draft_probs), _dev(probe_ids), n_probe,
+                                  ctypes.byref(fu), seed, _dev(accept_len), _dev(next_id), _stream(stream)))
 
 
 def rv_debug_output(cache: int, which: int, dst, stream=None) -> None:
@@ -272,8 +285,25 @@ class Verifier:
         self._keep = d_ids
         return lens
 
+    def verify_sampled(self, prefix_len, drafts, q, probe, alpha: float, prefix_pos: int, seed: int,
+                       temperature: float = 1.0):
+        """Algorithm 1's rule; q [batch][k][vocab] are the draft distributions."""
+        torch = self.torch
+        drafts = np.asarray(drafts, dtype=np.int32).reshape(self.batch, -1)
+        k = drafts.shape[1]
+        d_dr = torch.from_numpy(np.ascontiguousarray(drafts)).cuda()
+        d_q = torch.from_numpy(np.ascontiguousarray(np.asarray(q, dtype=np.float32))).cuda() if k else None
+        probe = np.asarray(probe, dtype=np.int32)
+        d_pr = torch.from_numpy(probe).cuda() if len(probe) else None
+        rv_verify_sampled(self.cache, prefix_len, d_dr, k, d_q, d_pr, len(probe), alpha, prefix_pos, seed,
+                          self.accept_len, self.next_id, temperature=temperature)
+        self._keep2 = (d_dr, d_pr, d_q)
+        self.k = k
+        return self.accept_len, self.next_id
+
     def verify(self, prefix_len, drafts, probe, alpha: float, prefix_pos: int, rule: int = RV_RULE_GREEDY,
-               epsilon: float = 0.09, delta: float = 0.3, entropy_src: int = RV_ENTROPY_FUSED):
+               epsilon: float = 0.09, delta: float = 0.3, entropy_src: int = RV_ENTROPY_FUSED,
+               temperature: float = 1.0):
         torch = self.torch
         drafts = np.asarray(drafts, dtype=np.int32).reshape(self.batch, -1)
         k = drafts.shape[1]
@@ -281,7 +311,8 @@ class Verifier:
         probe = np.asarray(probe, dtype=np.int32)
         d_pr = torch.from_numpy(probe).cuda() if len(probe) else None
         rv_verify(self.cache, prefix_len, d_dr, k, d_pr, len(probe), alpha, prefix_pos,
-                  self.accept_len, self.next_id, rule=rule, epsilon=epsilon, delta=delta, entropy_src=entropy_src)
+                  self.accept_len, self.next_id, rule=rule, epsilon=epsilon, delta=delta, entropy_src=entropy_src,
+                  temperature=temperature)
         self._keep2 = (d_dr, d_pr)
         self.k = k
         return self.accept_len, self.next_id

@@ -12,6 +12,12 @@
 //                    temperature 0) or the entropy-thresholded rule
 //                    (Algorithm 3), emits t = x_hat_{n+1} and appends
 //                    x_1..x_n, t to the id history.
+//                    With the sampling rule (Algorithm 1) it only decides
+//                    n, from Philox4x64-10 uniforms r_i.
+//  2b. k_sample, k_sample_finish   sampling rule: per vocabulary chunk the
+//                    best Gumbel-perturbed score of the residual
+//                    max(0, p_{n+1} - q_{n+1}) (or p_{k+1}); then per sequence
+//                    the chunk maxima merged in order give t.
 //  3. k_logprob      log-softmax rows of o, r and z (pass two).
 #include "rv_internal.h"
 
@@ -34,6 +40,32 @@ RV_DEV Top top_merge(Top a, Top b) {
   a.m2 = fmaxf(a.m2, b.m1);
   return a;
 }
+
+// Philox4x64-10 (Salmon et al., SC 2011): 10 rounds of two 64x64->128-bit
+// products of counter words 0 and 2 with fixed odd constants, mixed with the
+// other words and the key; the key advances by two Weyl constants between
+// rounds.
+RV_DEV void philox4x64(uint64_t (&c)[4], uint64_t k0, uint64_t k1) {
+  constexpr uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+  constexpr uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint64_t lo0 = M0 * c[0], hi0 = __umul64hi(M0, c[0]);
+    const uint64_t lo1 = M1 * c[2], hi1 = __umul64hi(M1, c[2]);
+    const uint64_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0;
+    c[1] = lo1;
+    c[2] = n2;
+    c[3] = lo0;
+    if (r < 9) {
+      k0 += W0;
+      k1 += W1;
+    }
+  }
+}
+
+// ((w >> 41) + 1/2) / 2^23: a uniform in (0, 1), exact in fp32.
+RV_DEV float uniform23(uint64_t w) { return ((float)(w >> 41) + 0.5f) * (1.0f / 8388608.0f); }
 
 // Softmax statistics of a set of values: max m, S = sum exp(x - m) and the
 // centred S1 = sum exp(x - m) (x - m).  Empty sets have m = -inf, S = S1 = 0.
@@ -103,11 +135,13 @@ __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
   // start from a valid id, so the argmax stays in the vocabulary even if
   // no value compares greater (NaN logits)
   Top t{-INFINITY, v0, -INFINITY};
+  const bool tempered = a.temp != 1.0f;
 #pragma unroll
   for (int e = 0; e < E; ++e) {
     const float zo = wo * ov[e];
     const float zr = wa * rv[e];
     zv[e] = zo + zr;
+    if (tempered) zv[e] = zv[e] / a.temp;
     if (e < n_valid) {
       const int v = v0 + threadIdx.x + e * 256;
       z[v] = zv[e];
@@ -219,6 +253,23 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
   }
   const int* x = a.drafts + (size_t)b * a.k;
   int n = a.k;
+  if (a.rule == RV_RULE_SAMPLING) {
+    // reject at the first r_i * q_i(x_i) > p_i(x_i); t is drawn by k_sample
+    for (int i = 0; i < a.k; ++i) {
+      uint64_t c[4] = {(uint64_t)i, (uint64_t)b, 0ull, 0ull};
+      philox4x64(c, a.seed, 0ull);
+      const float r = uniform23(c[0]);
+      const float p = expf(a.z[((size_t)b * k1 + i) * a.V + x[i]] - lse_z[i]);
+      const float qx = a.q[((size_t)b * a.k + i) * a.V + x[i]];
+      mg[i] = qx > 0.f ? logf(p) - logf(r * qx) : INFINITY;
+      if (r * qx > p) {
+        n = i;
+        break;
+      }
+    }
+    a.accept_len[b] = n;
+    return;
+  }
   if (a.rule == RV_RULE_TYPICAL) {
     // log p_i(x_i) > min(log eps, log delta - H_i)  (eps = inf, delta = 0 exact)
     const float log_eps = logf(a.eps), log_delta = logf(a.delta);
@@ -257,6 +308,94 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
   mg[a.k + 1] = a.z[((size_t)b * k1 + n) * a.V + t] - top2[n];
 }
 
+// Sampling rule: one workgroup per (vocabulary chunk, sequence).  Thread
+// tid owns the two groups of 4 consecutive ids 4*(tid + 256 u) (u < 2) of
+// the chunk, one Philox block each.  Writes the chunk's best perturbed
+// score, its lowest id and the runner-up to part plane 3 at the row of
+// position n+1.
+__global__ __launch_bounds__(256) void k_sample(HeadArgs a) {
+  const int chunk = blockIdx.x, b = blockIdx.y;
+  const int n = a.accept_len[b];
+  if (n < 0) return;
+  const int k1 = a.k + 1, R1 = a.B * k1, row = b * k1 + n;
+  const float* z = a.z + (size_t)row * a.V;
+  const float lse = a.lse[2 * R1 + row];
+  const float* q = n < a.k ? a.q + ((size_t)b * a.k + n) * a.V : nullptr;
+  const int v0 = chunk * a.chunk, v1 = min(a.V, v0 + a.chunk);
+  Top t{-INFINITY, v0, -INFINITY};
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int g0 = v0 + 4 * ((int)threadIdx.x + 256 * u);  // a multiple of 4
+    if (g0 >= v1) continue;
+    uint64_t c[4] = {(uint64_t)(g0 >> 2), (uint64_t)b, 1ull, 0ull};
+    philox4x64(c, a.seed, 0ull);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int v = g0 + j;
+      if (v >= v1) break;
+      const float lz = z[v] - lse;
+      float score;
+      if (q) {
+        const float w = expf(lz) - q[v];
+        score = w > 0.f ? logf(w) : -INFINITY;
+      } else {
+        score = lz;
+      }
+      const float s = score - logf(-logf(uniform23(c[j])));
+      if (s > t.m1) {
+        t.m2 = t.m1;
+        t.m1 = s;
+        t.i1 = v;
+      } else if (s > t.m2) {
+        t.m2 = s;
+      }
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    Top o{__shfl_xor(t.m1, off, 64), __shfl_xor(t.i1, off, 64), __shfl_xor(t.m2, off, 64)};
+    t = top_merge(t, o);
+  }
+  __shared__ Top sh[4];
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) sh[w] = t;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int ww = 1; ww < 4; ++ww) t = top_merge(t, sh[ww]);
+    float* p = a.part + ((size_t)(3 * R1 + row) * a.nchunk + chunk) * 4;
+    p[0] = __int_as_float(t.i1);
+    p[1] = t.m1;
+    p[2] = t.m2;
+  }
+}
+
+// Sampling rule, one wave per sequence: merges the chunk maxima (lane c
+// takes chunks c, c+64, ..., then a fixed butterfly), emits t and appends
+// x_1..x_n, t to the id history.
+__global__ __launch_bounds__(64) void k_sample_finish(HeadArgs a) {
+  const int b = blockIdx.x, lane = threadIdx.x;
+  const int n = a.accept_len[b];
+  if (n < 0) return;
+  const int k1 = a.k + 1, R1 = a.B * k1, row = b * k1 + n;
+  Top t{-INFINITY, 0x7fffffff, -INFINITY};
+  for (int c = lane; c < a.nchunk; c += 64) {
+    const float* p = a.part + ((size_t)(3 * R1 + row) * a.nchunk + c) * 4;
+    t = top_merge(t, Top{p[1], __float_as_int(p[0]), p[2]});
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    Top o{__shfl_xor(t.m1, off, 64), __shfl_xor(t.i1, off, 64), __shfl_xor(t.m2, off, 64)};
+    t = top_merge(t, o);
+  }
+  if (lane != 0) return;
+  const int tok = min(max(t.i1, 0), a.V - 1);
+  a.next_id[b] = tok;
+  const int* x = a.drafts + (size_t)b * a.k;
+  int* hist = a.ids + (size_t)b * a.max_len;
+  const int L = a.L[b];
+  for (int i = 0; i < n; ++i) hist[L + i] = x[i];
+  hist[L + n] = tok;
+  a.margins[(size_t)b * (a.k + 2) + a.k + 1] = t.m1 - t.m2;
+}
+
 __global__ __launch_bounds__(256) void k_logprob(HeadArgs a) {
   constexpr int E = 8;
   const int chunk = blockIdx.x, fr = blockIdx.y;  // fr = f * R1 + row
@@ -283,6 +422,10 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t st) {
   const int R1 = a.B * (a.k + 1);
   k_fuse_stats<<<dim3(a.nchunk, R1), 256, 0, st>>>(a);
   k_accept<<<a.B, 256, 0, st>>>(a);
+  if (a.rule == RV_RULE_SAMPLING) {
+    k_sample<<<dim3(a.nchunk, a.B), 256, 0, st>>>(a);
+    k_sample_finish<<<a.B, 64, 0, st>>>(a);
+  }
   k_logprob<<<dim3(a.nchunk, 3 * R1), 256, 0, st>>>(a);
   return hipGetLastError();
 }

@@ -751,18 +751,29 @@ rv_status rv_prefill_cache(rv_cache* c, const int32_t* d_prefix_ids, int32_t ld,
   return RV_OK;
 }
 
-rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t k,
-                    const int32_t* d_probe_ids, int32_t n_probe, const rv_fusion* fusion, int32_t* d_accept_len,
-                    int32_t* d_next_id, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// rv_verify and rv_verify_sampled: d_q / seed are used by the sampling rule only.
+rv_status verify_impl(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t k,
+                      const float* d_q, const int32_t* d_probe_ids, int32_t n_probe, const rv_fusion* fusion,
+                      uint64_t seed, bool sampled, int32_t* d_accept_len, int32_t* d_next_id, void* stream) {
   if (!c || !h_prefix_len || !fusion || !d_accept_len || !d_next_id)
     return fail(RV_E_ARG, "cache, prefix_len, fusion and outputs must not be NULL");
+  if (sampled != (fusion->rule == RV_RULE_SAMPLING))
+    return fail(RV_E_ARG, sampled ? "rv_verify_sampled needs rule RV_RULE_SAMPLING"
+                                  : "the sampling rule needs the draft distributions (rv_verify_sampled)");
+  if (sampled && k > 0 && !d_q) return fail(RV_E_ARG, "draft distributions are NULL");
+  if (!(fusion->temperature > 0.f && fusion->temperature < INFINITY))
+    return fail(RV_E_ARG, "temperature must be > 0 and finite");
   if (k < 0 || k > c->max_drafts) return fail(RV_E_ARG, "k = %d outside [0, max_drafts=%d]", k, c->max_drafts);
   if (k > 0 && !d_draft_ids) return fail(RV_E_ARG, "draft ids are NULL");
   if (n_probe < 0) return fail(RV_E_ARG, "n_probe must be >= 0");
   if (n_probe > 0 && !d_probe_ids) return fail(RV_E_ARG, "probe ids are NULL");
   if (!(fusion->alpha >= 0.f && fusion->alpha <= 1.f)) return fail(RV_E_ARG, "alpha must be in [0, 1]");
   if (fusion->prefix_pos < 0) return fail(RV_E_ARG, "prefix_pos must be >= 0");
-  if (fusion->rule != RV_RULE_GREEDY && fusion->rule != RV_RULE_TYPICAL)
+  if (fusion->rule != RV_RULE_GREEDY && fusion->rule != RV_RULE_TYPICAL && fusion->rule != RV_RULE_SAMPLING)
     return fail(RV_E_ARG, "unknown verification rule %d", fusion->rule);
   if (fusion->rule == RV_RULE_TYPICAL) {
     if (!(fusion->epsilon > 0.f)) return fail(RV_E_ARG, "epsilon must be > 0");
@@ -857,6 +868,9 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   ha.eps = fusion->epsilon;
   ha.delta = fusion->delta;
   ha.ent_src = fusion->entropy_src;
+  ha.temp = fusion->temperature;
+  ha.q = d_q;
+  ha.seed = seed;
   ha.entropy = c->entropy;
   ha.logits = c->logits;
   ha.z = c->z;
@@ -878,6 +892,25 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
   }
   c->last_k = k;
   return RV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t k,
+                    const int32_t* d_probe_ids, int32_t n_probe, const rv_fusion* fusion, int32_t* d_accept_len,
+                    int32_t* d_next_id, void* stream) {
+  return verify_impl(c, h_prefix_len, d_draft_ids, k, nullptr, d_probe_ids, n_probe, fusion, 0, false,
+                     d_accept_len, d_next_id, stream);
+}
+
+rv_status rv_verify_sampled(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t k,
+                            const float* d_draft_probs, const int32_t* d_probe_ids, int32_t n_probe,
+                            const rv_fusion* fusion, uint64_t seed, int32_t* d_accept_len,
+                            int32_t* d_next_id, void* stream) {
+  return verify_impl(c, h_prefix_len, d_draft_ids, k, d_draft_probs, d_probe_ids, n_probe, fusion, seed, true,
+                     d_accept_len, d_next_id, stream);
 }
 
 rv_status rv_debug_output(const rv_cache* c, int32_t which, float* d_dst, size_t dst_bytes, void* stream) {

@@ -173,6 +173,9 @@ struct HeadArgs {
   int rule;              // RV_RULE_GREEDY / RV_RULE_TYPICAL
   float eps, delta;      // typical threshold parameters
   int ent_src;           // RV_ENTROPY_FUSED / RV_ENTROPY_ORIGINAL
+  float temp;            // fused logits are divided by it (1: unchanged)
+  const float* q;        // sampling: draft distributions [B][k][V]
+  uint64_t seed;         // sampling: Philox key word 0
   const float* logits;   // [B][2(k+1)][V]: o rows then r rows per sequence
   float* z;              // [B][k+1][V]
   float* part;           // [4][B*(k+1)][nchunk][4]: (max, sum, centred sum) of o, r, z; z's top-2

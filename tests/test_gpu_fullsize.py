@@ -236,3 +236,41 @@ def test_full_8b_typical_rule_properties(rv, model8b, verify8b):
     torch.cuda.synchronize()
     z = model8b.output(rv.RV_OUT_FUSED).cpu().numpy()[0]
     assert (int(acc[0]), int(nxt[0])) == (w.k, int(np.argmax(z[w.k])))
+
+
+def test_full_8b_sampling_rule_properties(rv, model8b, verify8b):
+    """Algorithm 1's rule at the full 8B shape: with q equal to the fused
+    distribution every draft is accepted; with another q the decision equals
+    the rule applied to the GPU's own probabilities and the Philox uniforms."""
+    import torch
+    d = verify8b
+    w = d["w"]
+    V = SHAPE.vocab
+    drafts = list(d["greedy"][:w.k])
+    T = 0.8
+    # the fused distribution at temperature T, from a greedy-rule call
+    model8b.verify(d["lens"], np.array([drafts]), d["probe"], w.alpha, w.prefix_pos, temperature=T)
+    torch.cuda.synchronize()
+    lp = model8b.output(rv.RV_OUT_LOGP_FUSED).cpu().numpy()[0].astype(np.float64)
+    p = np.exp(lp)
+    acc, nxt = model8b.verify_sampled(d["lens"], np.array([drafts]), p[None, :w.k].astype(np.float32), d["probe"],
+                                      w.alpha, w.prefix_pos, 99, temperature=T)
+    torch.cuda.synchronize()
+    assert int(acc[0]) == w.k
+    # a flatter q: decisions from the GPU's own p and the same uniforms
+    q = (0.5 * p[:w.k] + 0.5 / V).astype(np.float32)
+    for seed in (1, 2, 3):
+        acc, nxt = model8b.verify_sampled(d["lens"], np.array([drafts]), q[None], d["probe"], w.alpha,
+                                          w.prefix_pos, seed, temperature=T)
+        torch.cuda.synchronize()
+        n = int(acc[0])
+        lp_s = model8b.output(rv.RV_OUT_LOGP_FUSED).cpu().numpy()[0].astype(np.float64)
+        margins = [lp_s[i][drafts[i]] - np.log(oracle.acceptance_uniform(seed, 0, i) * float(q[i][drafts[i]]))
+                   for i in range(w.k)]
+        n_ref = next((i for i, m in enumerate(margins) if m < 0), w.k)
+        if all(abs(m) > 1e-4 for m in margins[:n_ref + 1]):
+            assert n == n_ref, (seed, margins)
+        t = int(nxt[0])
+        assert 0 <= t < V
+        if n < w.k:  # the residual draw never picks a token with p <= q
+            assert np.exp(lp_s[n][t]) > q[n][t] * (1 - 1e-5)

@@ -165,6 +165,58 @@ def test_typical_rule_matches_oracle(rv, gpu, shape, alpha, typical):
     c.v.close()
 
 
+def sampling_case_q(shape, drafts, key, mass=0.4):
+    """Draft distributions that put `mass` on the draft token and spread the
+    rest by a random softmax (fp32, rows sum to 1)."""
+    rng = np.random.default_rng(key)
+    B, k = len(drafts), len(drafts[0])
+    lg = rng.standard_normal((B, k, shape.vocab)) * 2
+    q = np.exp(lg - lg.max(-1, keepdims=True))
+    q *= (1 - mass) / q.sum(-1, keepdims=True)
+    for b in range(B):
+        for i in range(k):
+            q[b, i, drafts[b][i]] += mass
+    return q.astype(np.float32)
+
+
+@pytest.mark.parametrize("shape", [workload.TINY, workload.TINY_GQA_BF16], ids=lambda s: s.name)
+@pytest.mark.parametrize("alpha,temperature,seed", [(0.3, 1.0, 7), (0.3, 0.05, 11), (1.0, 0.1, 12345678901234)])
+def test_sampling_rule_matches_oracle(rv, gpu, shape, alpha, temperature, seed):
+    """Algorithm 1's speculative-sampling rule against the oracle: same
+    Philox4x64-10 random numbers, same decisions unless near a tie."""
+    import torch
+    hists = [workload.random_ids(shape.vocab, L, 6, b) for b, L in enumerate([50, 81, 64])]
+    drafts = [draft_case(shape, 4, h, 4, 0.3, 70 + b) for b, h in enumerate(hists)]
+    probe = workload.random_ids(shape.vocab, 5, 6, 0xBEEF)
+    q = sampling_case_q(shape, drafts, seed % 1000)
+    k, P = 4, 3
+    S = 1 + 2 * k + len(probe) + P
+    v = rv.Verifier(shape, 4, len(hists), max(len(h) for h in hists) + S + 8, max_block=S, max_drafts=k)
+    lens = v.prefill([list(map(int, h)) for h in hists])
+    acc, nxt = v.verify_sampled(lens, np.array(drafts), q, probe, alpha, P, seed, temperature=temperature)
+    torch.cuda.synchronize()
+    acc, nxt = acc.cpu().numpy().copy(), nxt.cpu().numpy().copy()
+    z = v.output(rv.RV_OUT_FUSED).cpu().numpy()
+    mg = v.output(rv.RV_OUT_MARGINS).cpu().numpy()
+    decided = 0
+    for b in range(len(hists)):
+        ref = oracle.verify(shape, 4, list(map(int, hists[b])), drafts[b], probe, alpha, P, rule="sampling",
+                            temperature=temperature, q=q[b], rng_seed=seed, slot=b)
+        logits_close(shape, z[b], ref["z"])
+        if ref["near_tie"]:
+            continue
+        decided += 1
+        assert (int(acc[b]), int(nxt[b])) == (ref["accept_len"], ref["next_id"]), (b, ref["margins"], ref["gap"])
+        n_tested = len(ref["margins"])
+        np.testing.assert_allclose(mg[b][:n_tested], ref["margins"], atol=1e-3 if shape.dtype == "f32" else 5e-2)
+    assert decided >= 2
+    # the same call again: the same outputs (the draw is a function of the seed)
+    acc2, nxt2 = v.verify_sampled(lens, np.array(drafts), q, probe, alpha, P, seed, temperature=temperature)
+    torch.cuda.synchronize()
+    assert (acc2.cpu().numpy() == acc).all() and (nxt2.cpu().numpy() == nxt).all()
+    v.close()
+
+
 def test_kv_cache_matches_oracle(rv, gpu):
     """Prefill + verify write the KV the oracle computes at every position."""
     import torch
@@ -260,6 +312,23 @@ def test_validation_errors_enqueue_nothing(rv, gpu):
     assert code(epsilon=float("nan"), **typ) == "RV_E_ARG"
     assert code(delta=-0.1, **typ) == "RV_E_ARG"
     assert code(entropy_src=2, **typ) == "RV_E_ARG"
+    assert code(temperature=0.0) == "RV_E_ARG"
+    assert code(temperature=float("inf")) == "RV_E_ARG"
+    assert code(rule=rv.RV_RULE_SAMPLING) == "RV_E_ARG"  # needs the draft distributions
+    q = torch.full((1, 2, shape.vocab), 1.0 / shape.vocab, dtype=torch.float32, device="cuda")
+
+    def code_s(**kw):
+        args = dict(prefix_len=lens, draft_ids=d, k=2, draft_probs=q, probe_ids=probe, n_probe=3, alpha=0.3,
+                    prefix_pos=2, seed=1, accept_len=v.accept_len, next_id=v.next_id)
+        args.update(kw)
+        try:
+            rv.rv_verify_sampled(v.cache, **args)
+        except rv.RVError as e:
+            return e.name
+        return "RV_OK"
+
+    assert code_s(rule=rv.RV_RULE_GREEDY) == "RV_E_ARG"
+    assert code_s(draft_probs=None) == "RV_E_ARG"
     assert code(prefix_len=[1], prefix_pos=2) == "RV_E_RANGE"
     assert code(prefix_len=[41]) == "RV_E_RANGE"
     assert code(prefix_len=[35]) == "RV_E_CAPACITY"
