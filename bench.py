@@ -88,6 +88,47 @@ def calibrate_copy(nbytes=1 << 30, reps=3):
     print(json.dumps({"calibration_copy_bytes": nbytes, "reps": reps}), flush=True)
 
 
+def e2e_bench(args):
+    """End-to-end speculative decoding (the loop in paper_2505_18629_amd.spec_loop):
+    the 1B-shaped draft proposes k tokens one decode step at a time, the 8B target
+    verifies them in one reflective pass.  Both are random-init, so the draft
+    rarely matches the target: the figure is a timing of the loop, not of the
+    paper's acceptance rates (those need trained weights)."""
+    import torch
+    import paper_2505_18629_amd as rv
+    import workload as wl
+    from paper_2505_18629_amd.spec_loop import SpeculativeLoop
+    w = wl.WORKLOADS["8b-bf16-b1"]
+    lens = wl.prefix_lengths(w)
+    prefix = [int(t) for t in wl.prefix_ids(w, lens)[0]]
+    max_len = len(prefix) + (args.steps + args.warmup + 2) * (w.k + 1) + w.rows_per_seq + 8
+    tgt = rv.Verifier(w.shape, w.weight_seed, 1, max_len, max_block=max(64, w.rows_per_seq), max_drafts=w.k)
+    drf = rv.Verifier(wl.LLAMA1B, 1, 1, max_len, max_block=8, max_drafts=w.k)
+    loop = SpeculativeLoop(rv, tgt, drf, w.k, wl.probe_ids(w), w.alpha, w.prefix_pos)
+    loop.prefill([prefix])
+    for _ in range(args.warmup):
+        loop.round()
+    torch.cuda.synchronize()
+    n0, r0 = len(loop.tokens[0]), loop.rounds
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        loop.round()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    toks = len(loop.tokens[0]) - n0
+    print(json.dumps({
+        "metric": "end-to-end tokens/s (speculative loop, 1B-shaped draft + 8B-shaped target)",
+        "value": toks / wall, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_round": wall * 1e3 / args.steps, "higher_is_better": True, "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights and token ids)",
+        "config": {"workload": "8b-bf16-b1 target + llama3-1b-shaped draft", "k": w.k, "alpha": w.alpha,
+                   "rule": "greedy", "prefix_len": len(prefix)},
+        "mean_accepted": float(np.mean(loop.accepted[r0:])), "tokens": toks,
+    }), flush=True)
+    tgt.close()
+    drf.close()
+
+
 def source_hash(path):
     with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
@@ -185,6 +226,8 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=5)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration under rocprofv3)")
+    ap.add_argument("--e2e", action="store_true",
+                    help="time the end-to-end speculative loop (1B-shaped draft + 8B-shaped target) instead")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the verify pass shards by sequence "
@@ -193,6 +236,9 @@ def main():
 
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.e2e:
+        e2e_bench(args)
         return
 
     import torch

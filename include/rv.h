@@ -167,6 +167,14 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
                     const int32_t* d_probe_ids, int32_t n_probe, const rv_fusion* fusion,
                     int32_t* d_accept_len, int32_t* d_next_id, void* stream);
 
+/* Overwrites the id history: ids[b][h_pos[b]] = d_ids[b] for every sequence
+ * b with h_pos[b] >= 0 (host int32 [batch]; device int32 [batch]).  A
+ * speculative loop uses it to commit the token the target emitted into the
+ * draft model's cache (whose own history holds the draft token there); the
+ * next call on that cache then scores it as block row 0.  Positions must be
+ * < max_len.  Asynchronous. */
+rv_status rv_commit_tokens(rv_cache* c, const int32_t* h_pos, const int32_t* d_ids, void* stream);
+
 /* rv_verify with Algorithm 1's speculative-sampling rule (fusion->rule must
  * be RV_RULE_SAMPLING).
  *   d_draft_probs [batch][k][vocab] device fp32: the draft distributions q_i

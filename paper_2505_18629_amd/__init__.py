@@ -41,7 +41,7 @@ STATUS = {0: "RV_OK", -1: "RV_E_ARG", -2: "RV_E_RANGE", -3: "RV_E_CAPACITY", -4:
 
 EXPORTED = [
     "rv_status_str", "rv_last_error", "rv_model_bytes", "rv_init_weights", "rv_model_free",
-    "rv_cache_bytes", "rv_cache_create", "rv_cache_free", "rv_prefill_cache", "rv_verify", "rv_verify_sampled",
+    "rv_cache_bytes", "rv_cache_create", "rv_cache_free", "rv_prefill_cache", "rv_verify", "rv_verify_sampled", "rv_commit_tokens",
     "rv_debug_output", "rv_debug_export_kv", "rv_debug_export_ids", "rv_debug_weight_bits",
     "rv_debug_linear", "rv_debug_workspace", "rv_debug_profile", "rv_debug_profile_read", "rv_debug_time_matrix",
 ]
@@ -82,6 +82,7 @@ _sig = {
     "rv_verify": ([_vp, _P_i32, _vp, _i32, _vp, _i32, ctypes.POINTER(rv_fusion), _vp, _vp, _vp], ctypes.c_int),
     "rv_verify_sampled": ([_vp, _P_i32, _vp, _i32, _vp, _vp, _i32, ctypes.POINTER(rv_fusion), ctypes.c_uint64, _vp,
                            _vp, _vp], ctypes.c_int),
+    "rv_commit_tokens": ([_vp, _P_i32, _vp, _vp], ctypes.c_int),
     "rv_debug_output": ([_vp, _i32, _vp, _sz, _vp], ctypes.c_int),
     "rv_debug_export_kv": ([_vp, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp], ctypes.c_int),
     "rv_debug_export_ids": ([_vp, _i32, _i32, _i32, _vp, _vp], ctypes.c_int),
@@ -198,6 +199,11 @@ def rv_verify_sampled(cache: int, prefix_len: Sequence[int], draft_ids, k: int, 
     fu = rv_fusion(alpha, prefix_pos, rule, 0.0, 0.0, RV_ENTROPY_FUSED, temperature)
     _check(_lib.rv_verify_sampled(cache, lens, _dev(draft_ids), k, _dev(draft_probs), _dev(probe_ids), n_probe,
                                   ctypes.byref(fu), seed, _dev(accept_len), _dev(next_id), _stream(stream)))
+
+
+def rv_commit_tokens(cache: int, positions: Sequence[int], ids, stream=None) -> None:
+    _keep, pos = _host_i32(positions)
+    _check(_lib.rv_commit_tokens(cache, pos, _dev(ids), _stream(stream)))
 
 
 def rv_debug_output(cache: int, which: int, dst, stream=None) -> None:

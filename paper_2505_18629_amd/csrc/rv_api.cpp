@@ -968,6 +968,19 @@ rv_status rv_debug_export_kv(const rv_cache* c, int32_t layer, int32_t seq, int3
   return RV_OK;
 }
 
+rv_status rv_commit_tokens(rv_cache* c, const int32_t* h_pos, const int32_t* d_ids, void* stream) {
+  if (!c || !h_pos || !d_ids) return fail(RV_E_ARG, "cache, positions and ids must not be NULL");
+  for (int b = 0; b < c->B; ++b)
+    if (h_pos[b] >= c->max_len) return fail(RV_E_RANGE, "position %d of sequence %d >= max_len", h_pos[b], b);
+  for (int b = 0; b < c->B; ++b) {
+    if (h_pos[b] < 0) continue;
+    HIP_TRY(hipMemcpyAsync(c->ids + (size_t)b * c->max_len + h_pos[b], d_ids + b, 4, hipMemcpyDeviceToDevice,
+                           (hipStream_t)stream),
+            "copy");
+  }
+  return RV_OK;
+}
+
 rv_status rv_debug_export_ids(const rv_cache* c, int32_t seq, int32_t pos0, int32_t n, int32_t* d_dst, void* stream) {
   if (!c || !d_dst) return fail(RV_E_ARG, "cache and destination must not be NULL");
   if (seq < 0 || seq >= c->B || pos0 < 0 || n <= 0 || (long long)pos0 + n > c->max_len)

@@ -41,6 +41,8 @@ class ModelShape:
 
 TINY = ModelShape("tiny", 2, 256, 4, 4, 64, 1024, 4096, "f32")
 LLAMA8B = ModelShape("llama3-8b", 32, 4096, 32, 8, 128, 14336, 128256, "bf16")
+# the 1B draft paired with the 8B target (Section 4.1): Llama-3.2-1B's shape
+LLAMA1B = ModelShape("llama3-1b", 16, 2048, 32, 8, 64, 8192, 128256, "bf16")
 QWEN14B = ModelShape("14b", 48, 5120, 40, 8, 128, 13824, 152064, "bf16")
 LLAMA70B = ModelShape("llama3-70b", 80, 8192, 64, 8, 128, 28672, 128256, "bf16")
 # small bf16 shape with GQA for quick parity cases
