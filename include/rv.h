@@ -167,6 +167,19 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
                     const int32_t* d_probe_ids, int32_t n_probe, const rv_fusion* fusion,
                     int32_t* d_accept_len, int32_t* d_next_id, void* stream);
 
+/* rv_verify with a draft count per sequence (dynamic draft length).
+ *   d_draft_ids [batch][ld_drafts] device int32; sequence b uses its first
+ *               h_draft_len[b] entries (0 <= h_draft_len[b] <= ld_drafts <=
+ *               max_drafts).
+ *   h_draft_len [batch] host int32.
+ * Sequence b's block has S_b = 1 + 2 k_b + n_probe + P rows; the probe, P,
+ * alpha and the rule (RV_RULE_GREEDY or RV_RULE_TYPICAL) are shared.
+ * Per-row debug outputs then hold sum_b (k_b + 1) rows, sequence after
+ * sequence.  Everything else as rv_verify. */
+rv_status rv_verify_ragged(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t ld_drafts,
+                           const int32_t* h_draft_len, const int32_t* d_probe_ids, int32_t n_probe,
+                           const rv_fusion* fusion, int32_t* d_accept_len, int32_t* d_next_id, void* stream);
+
 /* Overwrites the id history: ids[b][h_pos[b]] = d_ids[b] for every sequence
  * b with h_pos[b] >= 0 (host int32 [batch]; device int32 [batch]).  A
  * speculative loop uses it to commit the token the target emitted into the
@@ -197,14 +210,16 @@ rv_status rv_verify_sampled(rv_cache* c, const int32_t* h_prefix_len, const int3
 
 /* ---- inspection (tests and benchmarks) ---- */
 
-/* Which result of the last rv_verify to copy.  RV_OUT_ORIG .. RV_OUT_LOGP_FUSED
- * are fp32 [batch][k+1][vocab]: raw logits o_i and r_i, fused logits z_i,
- * and their log-softmax (natural log).  RV_OUT_ENTROPY is fp32
- * [2][batch][k+1]: the entropy (nats) of softmax(z_i), then of softmax(o_i).
- * RV_OUT_MARGINS is fp32 [batch][k+2]: for each tested draft the distance of
+/* Which result of the last verify to copy.  Per-row results have one row per
+ * (sequence b, i = 1..k_b+1), sequence after sequence ([batch][k+1] when every
+ * sequence has k drafts).  RV_OUT_ORIG .. RV_OUT_LOGP_FUSED are fp32 rows of
+ * vocab entries: raw logits o_i and r_i, fused logits z_i, and their
+ * log-softmax (natural log).  RV_OUT_ENTROPY is fp32 [2][rows]: the entropy
+ * (nats) of softmax(z_i), then of softmax(o_i).  RV_OUT_MARGINS is fp32
+ * [batch][k+2] (k the draft-id stride): for each tested draft the distance of
  * its decision from the boundary (greedy: z_i[x_i] - max_{v != x_i} z_i[v];
  * typical: log p_i(x_i) - log threshold_i; sampling: log p_i(x_i) -
- * log(r_i q_i(x_i)); NaN for untested drafts), then NaN, then the top-1
+ * log(r_i q_i(x_i)); NaN for untested drafts), NaN, and last the top-1
  * minus top-2 gap of z_{n+1} (sampling: of the perturbed draw scores). */
 enum {
   RV_OUT_ORIG = 0, RV_OUT_REFL = 1, RV_OUT_FUSED = 2,

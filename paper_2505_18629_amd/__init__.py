@@ -41,7 +41,7 @@ STATUS = {0: "RV_OK", -1: "RV_E_ARG", -2: "RV_E_RANGE", -3: "RV_E_CAPACITY", -4:
 
 EXPORTED = [
     "rv_status_str", "rv_last_error", "rv_model_bytes", "rv_init_weights", "rv_model_free",
-    "rv_cache_bytes", "rv_cache_create", "rv_cache_free", "rv_prefill_cache", "rv_verify", "rv_verify_sampled", "rv_commit_tokens",
+    "rv_cache_bytes", "rv_cache_create", "rv_cache_free", "rv_prefill_cache", "rv_verify", "rv_verify_sampled", "rv_verify_ragged", "rv_commit_tokens",
     "rv_debug_output", "rv_debug_export_kv", "rv_debug_export_ids", "rv_debug_weight_bits",
     "rv_debug_linear", "rv_debug_workspace", "rv_debug_profile", "rv_debug_profile_read", "rv_debug_time_matrix",
 ]
@@ -83,6 +83,8 @@ _sig = {
     "rv_verify_sampled": ([_vp, _P_i32, _vp, _i32, _vp, _vp, _i32, ctypes.POINTER(rv_fusion), ctypes.c_uint64, _vp,
                            _vp, _vp], ctypes.c_int),
     "rv_commit_tokens": ([_vp, _P_i32, _vp, _vp], ctypes.c_int),
+    "rv_verify_ragged": ([_vp, _P_i32, _vp, _i32, _P_i32, _vp, _i32, ctypes.POINTER(rv_fusion), _vp, _vp, _vp],
+                         ctypes.c_int),
     "rv_debug_output": ([_vp, _i32, _vp, _sz, _vp], ctypes.c_int),
     "rv_debug_export_kv": ([_vp, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp], ctypes.c_int),
     "rv_debug_export_ids": ([_vp, _i32, _i32, _i32, _vp, _vp], ctypes.c_int),
@@ -201,6 +203,17 @@ def rv_verify_sampled(cache: int, prefix_len: Sequence[int], draft_ids, k: int, 
                                   ctypes.byref(fu), seed, _dev(accept_len), _dev(next_id), _stream(stream)))
 
 
+def rv_verify_ragged(cache: int, prefix_len: Sequence[int], draft_ids, ld_drafts: int, draft_len: Sequence[int],
+                     probe_ids, n_probe: int, alpha: float, prefix_pos: int, accept_len, next_id,
+                     rule: int = RV_RULE_GREEDY, epsilon: float = 0.09, delta: float = 0.3,
+                     entropy_src: int = RV_ENTROPY_FUSED, temperature: float = 1.0, stream=None) -> None:
+    _keep, lens = _host_i32(prefix_len)
+    _keep2, kl = _host_i32(draft_len)
+    fu = rv_fusion(alpha, prefix_pos, rule, epsilon, delta, entropy_src, temperature)
+    _check(_lib.rv_verify_ragged(cache, lens, _dev(draft_ids), ld_drafts, kl, _dev(probe_ids), n_probe,
+                                 ctypes.byref(fu), _dev(accept_len), _dev(next_id), _stream(stream)))
+
+
 def rv_commit_tokens(cache: int, positions: Sequence[int], ids, stream=None) -> None:
     _keep, pos = _host_i32(positions)
     _check(_lib.rv_commit_tokens(cache, pos, _dev(ids), _stream(stream)))
@@ -291,6 +304,24 @@ class Verifier:
         self._keep = d_ids
         return lens
 
+    def verify_ragged(self, prefix_len, drafts: Sequence[Sequence[int]], probe, alpha: float, prefix_pos: int,
+                      **kw):
+        """One draft list per sequence (lengths may differ)."""
+        torch = self.torch
+        kl = [len(d) for d in drafts]
+        ld = max(max(kl), 1)
+        pad = np.zeros((self.batch, ld), dtype=np.int32)
+        for b, d in enumerate(drafts):
+            pad[b, :len(d)] = d
+        d_dr = torch.from_numpy(pad).cuda()
+        probe = np.asarray(probe, dtype=np.int32)
+        d_pr = torch.from_numpy(probe).cuda() if len(probe) else None
+        rv_verify_ragged(self.cache, prefix_len, d_dr, ld, kl, d_pr, len(probe), alpha, prefix_pos,
+                         self.accept_len, self.next_id, **kw)
+        self._keep2 = (d_dr, d_pr)
+        self.k, self.kb = ld, kl
+        return self.accept_len, self.next_id
+
     def verify_sampled(self, prefix_len, drafts, q, probe, alpha: float, prefix_pos: int, seed: int,
                        temperature: float = 1.0):
         """Algorithm 1's rule; q [batch][k][vocab] are the draft distributions."""
@@ -304,7 +335,7 @@ class Verifier:
         rv_verify_sampled(self.cache, prefix_len, d_dr, k, d_q, d_pr, len(probe), alpha, prefix_pos, seed,
                           self.accept_len, self.next_id, temperature=temperature)
         self._keep2 = (d_dr, d_pr, d_q)
-        self.k = k
+        self.k, self.kb = k, None
         return self.accept_len, self.next_id
 
     def verify(self, prefix_len, drafts, probe, alpha: float, prefix_pos: int, rule: int = RV_RULE_GREEDY,
@@ -320,17 +351,20 @@ class Verifier:
                   self.accept_len, self.next_id, rule=rule, epsilon=epsilon, delta=delta, entropy_src=entropy_src,
                   temperature=temperature)
         self._keep2 = (d_dr, d_pr)
-        self.k = k
+        self.k, self.kb = k, None
         return self.accept_len, self.next_id
 
     def output(self, which: int):
+        """Uniform draft counts: [batch][k+1] rows; ragged (verify_ragged):
+        [sum(k_b+1)] rows, sequence after sequence."""
         torch = self.torch
+        rows = (self.batch, self.k + 1) if getattr(self, "kb", None) is None else (sum(k + 1 for k in self.kb),)
         if which == RV_OUT_ENTROPY:
-            shape = (2, self.batch, self.k + 1)
+            shape = (2,) + rows
         elif which == RV_OUT_MARGINS:
             shape = (self.batch, self.k + 2)
         else:
-            shape = (self.batch, self.k + 1, self.shape.vocab)
+            shape = rows + (self.shape.vocab,)
         out = torch.empty(shape, dtype=torch.float32, device="cuda")
         rv_debug_output(self.cache, which, out)
         return out

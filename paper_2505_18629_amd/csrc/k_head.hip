@@ -67,6 +67,18 @@ RV_DEV void philox4x64(uint64_t (&c)[4], uint64_t k0, uint64_t k1) {
 // ((w >> 41) + 1/2) / 2^23: a uniform in (0, 1), exact in fp32.
 RV_DEV float uniform23(uint64_t w) { return ((float)(w >> 41) + 0.5f) * (1.0f / 8388608.0f); }
 
+// Sequence b of fused row r and the row's index i within it (sequence b owns
+// rows b + K_b .. b + K_b + k_b).
+RV_DEV void fused_row_seq(const uint8_t* kb, int B, int r, int& b, int& i) {
+  int start = 0;
+  for (b = 0; b < B - 1; ++b) {
+    const int n = kb[b] + 1;
+    if (r < start + n) break;
+    start += n;
+  }
+  i = r - start;
+}
+
 // Softmax statistics of a set of values: max m, S = sum exp(x - m) and the
 // centred S1 = sum exp(x - m) (x - m).  Empty sets have m = -inf, S = S1 = 0.
 struct Stat {
@@ -116,10 +128,12 @@ RV_DEV Stat stat_of(const float (&x)[E], int n_valid) {
 // entries, strided by 256, and loads them all before computing.
 __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
   constexpr int E = 8;
-  const int chunk = blockIdx.x, row = blockIdx.y;  // row = b*(k+1) + i
-  const int k1 = a.k + 1, b = row / k1, i = row % k1;
-  const float* o = a.logits + ((size_t)b * 2 * k1 + i) * a.V;
-  const float* r = a.logits + ((size_t)b * 2 * k1 + k1 + i) * a.V;
+  const int chunk = blockIdx.x, row = blockIdx.y;  // fused row
+  int b, i;
+  fused_row_seq(a.kb, a.B, row, b, i);
+  const int k1 = a.kb[b] + 1, lrow0 = 2 * (row - i);  // first logit row of sequence b
+  const float* o = a.logits + ((size_t)lrow0 + i) * a.V;
+  const float* r = a.logits + ((size_t)lrow0 + k1 + i) * a.V;
   float* z = a.z + (size_t)row * a.V;
   const float wa = a.alpha, wo = 1.0f - a.alpha;
   const int v0 = chunk * a.chunk, v1 = min(a.V, v0 + a.chunk);
@@ -180,7 +194,7 @@ __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
       sz = stat_merge(sz, sh_st[ww][2]);
       t = top_merge(t, sh_top[ww]);
     }
-    const int R1 = a.B * k1;
+    const int R1 = a.R1;
     const Stat st[3] = {so, sr, sz};
     for (int f = 0; f < 3; ++f) {
       float* p = a.part + ((size_t)(f * R1 + row) * a.nchunk + chunk) * 4;
@@ -202,13 +216,14 @@ __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
 // merges lanes in a fixed butterfly order.  Thread 0 then applies the rule.
 __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
   const int b = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  const int k1 = a.k + 1, R1 = a.B * k1;
+  const int kb = a.kb[b], k1 = kb + 1, R1 = a.R1, Kb = kb_prefix(a.kb, b);
+  const int zrow0 = b + Kb;  // first fused row of sequence b
   __shared__ int xhat[RV_MAX_DRAFTS + 1];
   __shared__ float top2[RV_MAX_DRAFTS + 1];
   __shared__ float lse_z[RV_MAX_DRAFTS + 1];
   __shared__ float ent[2][RV_MAX_DRAFTS + 1];
   for (int i = w; i < k1; i += 4) {
-    const int row = b * k1 + i;
+    const int row = zrow0 + i;
     Stat st[3] = {{-INFINITY, 0.f, 0.f}, {-INFINITY, 0.f, 0.f}, {-INFINITY, 0.f, 0.f}};
     Top t{-INFINITY, 0x7fffffff, -INFINITY};
     for (int c = lane; c < a.nchunk; c += 64) {
@@ -243,7 +258,8 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
   __syncthreads();
   if (threadIdx.x != 0) return;
   int bad = a.seq_bad[b];
-  for (int j = 0; j < a.S; ++j) bad |= a.row_bad[b * a.S + j];
+  const int S = 1 + 2 * kb + a.n_probe + a.P, brow0 = b * (1 + a.n_probe + a.P) + 2 * Kb;
+  for (int j = 0; j < S; ++j) bad |= a.row_bad[brow0 + j];
   float* mg = a.margins + (size_t)b * (a.k + 2);
   for (int i = 0; i < a.k + 2; ++i) mg[i] = NAN;
   if (bad) {
@@ -252,14 +268,14 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
     return;
   }
   const int* x = a.drafts + (size_t)b * a.k;
-  int n = a.k;
+  int n = kb;
   if (a.rule == RV_RULE_SAMPLING) {
     // reject at the first r_i * q_i(x_i) > p_i(x_i); t is drawn by k_sample
-    for (int i = 0; i < a.k; ++i) {
+    for (int i = 0; i < kb; ++i) {
       uint64_t c[4] = {(uint64_t)i, (uint64_t)b, 0ull, 0ull};
       philox4x64(c, a.seed, 0ull);
       const float r = uniform23(c[0]);
-      const float p = expf(a.z[((size_t)b * k1 + i) * a.V + x[i]] - lse_z[i]);
+      const float p = expf(a.z[((size_t)zrow0 + i) * a.V + x[i]] - lse_z[i]);
       const float qx = a.q[((size_t)b * a.k + i) * a.V + x[i]];
       mg[i] = qx > 0.f ? logf(p) - logf(r * qx) : INFINITY;
       if (r * qx > p) {
@@ -274,8 +290,8 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
     // log p_i(x_i) > min(log eps, log delta - H_i)  (eps = inf, delta = 0 exact)
     const float log_eps = logf(a.eps), log_delta = logf(a.delta);
     const int src = a.ent_src == RV_ENTROPY_ORIGINAL ? 1 : 0;
-    for (int i = 0; i < a.k; ++i) {
-      const float lp = a.z[((size_t)b * k1 + i) * a.V + x[i]] - lse_z[i];
+    for (int i = 0; i < kb; ++i) {
+      const float lp = a.z[((size_t)zrow0 + i) * a.V + x[i]] - lse_z[i];
       const float m = lp - fminf(log_eps, log_delta - ent[src][i]);
       mg[i] = m;
       if (!(m > 0.f)) {
@@ -284,15 +300,15 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
       }
     }
   } else {
-    for (int i = 0; i < a.k; ++i) {
+    for (int i = 0; i < kb; ++i) {
       if (xhat[i] != x[i]) {
         n = i;
         break;
       }
     }
     // margins of the tested drafts (inspection only)
-    for (int i = 0; i < min(n + 1, a.k); ++i) {
-      const float* zi = a.z + ((size_t)b * k1 + i) * a.V;
+    for (int i = 0; i < min(n + 1, kb); ++i) {
+      const float* zi = a.z + ((size_t)zrow0 + i) * a.V;
       const float zx = zi[x[i]];
       mg[i] = xhat[i] == x[i] ? zx - top2[i] : zx - zi[xhat[i]];
     }
@@ -305,7 +321,7 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
   for (int i = 0; i < n; ++i) hist[L + i] = x[i];
   hist[L + n] = t;
   // bonus-token gap
-  mg[a.k + 1] = a.z[((size_t)b * k1 + n) * a.V + t] - top2[n];
+  mg[a.k + 1] = a.z[((size_t)zrow0 + n) * a.V + t] - top2[n];
 }
 
 // Sampling rule: one workgroup per (vocabulary chunk, sequence).  Thread
@@ -317,10 +333,10 @@ __global__ __launch_bounds__(256) void k_sample(HeadArgs a) {
   const int chunk = blockIdx.x, b = blockIdx.y;
   const int n = a.accept_len[b];
   if (n < 0) return;
-  const int k1 = a.k + 1, R1 = a.B * k1, row = b * k1 + n;
+  const int R1 = a.R1, row = b + kb_prefix(a.kb, b) + n;
   const float* z = a.z + (size_t)row * a.V;
   const float lse = a.lse[2 * R1 + row];
-  const float* q = n < a.k ? a.q + ((size_t)b * a.k + n) * a.V : nullptr;
+  const float* q = n < a.kb[b] ? a.q + ((size_t)b * a.k + n) * a.V : nullptr;
   const int v0 = chunk * a.chunk, v1 = min(a.V, v0 + a.chunk);
   Top t{-INFINITY, v0, -INFINITY};
 #pragma unroll
@@ -375,7 +391,7 @@ __global__ __launch_bounds__(64) void k_sample_finish(HeadArgs a) {
   const int b = blockIdx.x, lane = threadIdx.x;
   const int n = a.accept_len[b];
   if (n < 0) return;
-  const int k1 = a.k + 1, R1 = a.B * k1, row = b * k1 + n;
+  const int R1 = a.R1, row = b + kb_prefix(a.kb, b) + n;
   Top t{-INFINITY, 0x7fffffff, -INFINITY};
   for (int c = lane; c < a.nchunk; c += 64) {
     const float* p = a.part + ((size_t)(3 * R1 + row) * a.nchunk + c) * 4;
@@ -399,10 +415,13 @@ __global__ __launch_bounds__(64) void k_sample_finish(HeadArgs a) {
 __global__ __launch_bounds__(256) void k_logprob(HeadArgs a) {
   constexpr int E = 8;
   const int chunk = blockIdx.x, fr = blockIdx.y;  // fr = f * R1 + row
-  const int k1 = a.k + 1, R1 = a.B * k1;
-  const int f = fr / R1, row = fr % R1, b = row / k1, i = row % k1;
+  const int R1 = a.R1;
+  const int f = fr / R1, row = fr % R1;
+  int b, i;
+  fused_row_seq(a.kb, a.B, row, b, i);
+  const int k1 = a.kb[b] + 1;
   const float* src = f == 2 ? a.z + (size_t)row * a.V
-                            : a.logits + ((size_t)b * 2 * k1 + (f == 1 ? k1 : 0) + i) * a.V;
+                            : a.logits + ((size_t)2 * (row - i) + (f == 1 ? k1 : 0) + i) * a.V;
   float* dst = a.lp + (size_t)fr * a.V;
   const float l = a.lse[fr];
   const int v0 = chunk * a.chunk, v1 = min(a.V, v0 + a.chunk);
@@ -419,7 +438,7 @@ __global__ __launch_bounds__(256) void k_logprob(HeadArgs a) {
 }  // namespace
 
 hipError_t launch_head(const HeadArgs& a, hipStream_t st) {
-  const int R1 = a.B * (a.k + 1);
+  const int R1 = a.R1;
   k_fuse_stats<<<dim3(a.nchunk, R1), 256, 0, st>>>(a);
   k_accept<<<a.B, 256, 0, st>>>(a);
   if (a.rule == RV_RULE_SAMPLING) {

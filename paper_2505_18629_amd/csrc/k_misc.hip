@@ -13,14 +13,11 @@ namespace {
 // using any of them.
 template <int DT, int NPT>
 __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, const float* __restrict__ gain,
-                                                  float eps, void* __restrict__ out, void* __restrict__ out2, int gS,
-                                                  int gk, int gshift, const float* __restrict__ P, int pk, int prows) {
+                                                  float eps, void* __restrict__ out, void* __restrict__ out2,
+                                                  const int* __restrict__ gather, const float* __restrict__ P,
+                                                  int pk, int prows) {
   const int r = blockIdx.x;
-  int src = r;
-  if (gk >= 0) {
-    const int per = 2 * (gk + 1), b = r / per, j = r % per;
-    src = b * gS + (j <= gk ? j : gshift + j - (gk + 1));
-  }
+  const int src = gather ? gather[r] : r;
   float* x = h + (size_t)src * d;
   f32x4_t v[NPT];
 #pragma unroll
@@ -154,15 +151,20 @@ RV_DEV void gather_row(const typename Tr<DT>::T* embed, int tok, int d, float* d
 template <int DT>
 __global__ __launch_bounds__(256) void k_plan_verify(PlanVerify p) {
   const int j = blockIdx.x, b = blockIdx.y;
+  const int k = p.kb[b], S = 1 + 2 * k + p.n_probe + p.P;
+  if (j >= S) return;
+  const int Kb = kb_prefix(p.kb, b);
+  const int row0 = b * (1 + p.n_probe + p.P) + 2 * Kb;  // first block row of sequence b
   const int L = p.L[b];
   const int* hist = p.ids + (size_t)b * p.max_len;
+  const int* x = p.drafts + (size_t)b * p.k;
   int tok;
   if (j == 0) tok = hist[L - 1];
-  else if (j <= p.k) tok = p.drafts[b * p.k + j - 1];
-  else if (j <= p.k + p.n_probe) tok = p.probe[j - p.k - 1];
-  else if (j <= p.k + p.n_probe + p.P) tok = hist[L - p.P + (j - p.k - p.n_probe - 1)];
-  else tok = p.drafts[b * p.k + (j - p.k - p.n_probe - p.P - 1)];
-  const int row = b * p.S + j;
+  else if (j <= k) tok = x[j - 1];
+  else if (j <= k + p.n_probe) tok = p.probe[j - k - 1];
+  else if (j <= k + p.n_probe + p.P) tok = hist[L - p.P + (j - k - p.n_probe - 1)];
+  else tok = x[j - k - p.n_probe - p.P - 1];
+  const int row = row0 + j;
   const bool bad = tok < 0 || tok >= p.V;
   if (threadIdx.x == 0) {
     p.row_pos[row] = L - 1 + j;
@@ -170,10 +172,15 @@ __global__ __launch_bounds__(256) void k_plan_verify(PlanVerify p) {
     p.row_bad[row] = bad ? 1 : 0;
     if (j == 0) {
       p.seg_b[b] = b;
-      p.seg_row0[b] = b * p.S;
-      p.seg_n[b] = p.S;
+      p.seg_row0[b] = row0;
+      p.seg_n[b] = S;
       p.seg_pos0[b] = L - 1;
     }
+    // LM-head rows of sequence b: o_1..o_{k+1} = block rows 0..k, then
+    // r_1..r_{k+1} = rows shift..shift+k (shift = k + n_probe + P)
+    const int lrow0 = 2 * (b + Kb), shift = k + p.n_probe + p.P;
+    if (j <= k) p.lm_src[lrow0 + j] = row;
+    if (j >= shift && j <= shift + k) p.lm_src[lrow0 + k + 1 + (j - shift)] = row;
   }
   gather_row<DT>((const typename Tr<DT>::T*)p.embed, bad ? 0 : tok, p.d, p.h + (size_t)row * p.d);
 }
@@ -217,15 +224,14 @@ __global__ __launch_bounds__(256) void k_store_ids(StoreIds s) {
 }  // namespace
 
 hipError_t launch_rmsnorm(int dtype, float* h, int rows, int d, const float* gain, float eps, void* out,
-                          void* out2, int gS, int gk, int gshift, const float* P, int pk, int prows,
-                          hipStream_t st) {
+                          void* out2, const int* gather, const float* P, int pk, int prows, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   // d is a multiple of 128: one float4 per thread up to d = 4096, else two
   const int npt = d <= 4096 ? 1 : 2;
   const int threads = d / (4 * npt);
   if (threads > 1024 || threads % 64) return hipErrorInvalidValue;
 #define RV_NORM(DT_, N_) \
-  k_rmsnorm<DT_, N_><<<rows, threads, 0, st>>>(h, d, gain, eps, out, out2, gS, gk, gshift, P, pk, prows)
+  k_rmsnorm<DT_, N_><<<rows, threads, 0, st>>>(h, d, gain, eps, out, out2, gather, P, pk, prows)
   if (dtype == RV_BF16) {
     if (npt == 1) RV_NORM(RV_BF16, 1); else RV_NORM(RV_BF16, 2);
   } else {

@@ -104,6 +104,9 @@ struct rv_cache {
   float* gpart;  // k-group partials of a split matmul [gk][rows][max(d_model, qkv rows)], gk*rows <= gpart_rows
   int gpart_rows;
   float *logits, *z, *lp, *hpart, *lse, *margins, *entropy;
+  int* lm_src;                      // block row of each LM-head row of the last verify
+  int last_R1;                      // fused rows of the last verify
+  uint8_t last_kb[RV_MAX_BATCH];    // its per-sequence draft counts
   int* argmax;
   int last_k = -1;
   // event profiler
@@ -227,6 +230,7 @@ size_t cache_layout(rv_cache* c, void* buf) {
   c->lse = cv.take<float*>((size_t)3 * c->r1_cap * 4);
   c->margins = cv.take<float*>((size_t)c->B * (c->max_drafts + 2) * 4);
   c->entropy = cv.take<float*>((size_t)2 * c->r1_cap * 4);
+  c->lm_src = cv.take<int*>((size_t)c->out_rows_cap * 4);
   c->argmax = cv.take<int*>((size_t)c->r1_cap * 4);
   return align_up(cv.off, kAlign);
 }
@@ -405,7 +409,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, b
     char* vc2 = m->es == 2 ? c->vc2 + lo : nullptr;
     {
       Prof pf(c, RV_PROF_NORM, st);
-      HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n1[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0,
+      HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n1[l], mc.rms_eps, c->xn, c->xn2, nullptr,
                              pending > 1 ? c->gpart : nullptr, pending, M, st),
               "rmsnorm");
     }
@@ -481,7 +485,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, b
 
     {
       Prof pf(c, RV_PROF_NORM, st);
-      HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n2[l], mc.rms_eps, c->xn, c->xn2, 0, -1, 0,
+      HIP_TRY(launch_rmsnorm(dt, c->h, M, d, m->n2[l], mc.rms_eps, c->xn, c->xn2, nullptr,
                              pending > 1 ? c->gpart : nullptr, pending, M, st),
               "rmsnorm");
     }
@@ -756,9 +760,12 @@ rv_status rv_prefill_cache(rv_cache* c, const int32_t* d_prefix_ids, int32_t ld,
 namespace {
 
 // rv_verify and rv_verify_sampled: d_q / seed are used by the sampling rule only.
+// k is the draft-id stride and largest draft count; h_draft_len (may be NULL:
+// every sequence has k drafts) gives per-sequence counts.
 rv_status verify_impl(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t k,
-                      const float* d_q, const int32_t* d_probe_ids, int32_t n_probe, const rv_fusion* fusion,
-                      uint64_t seed, bool sampled, int32_t* d_accept_len, int32_t* d_next_id, void* stream) {
+                      const int32_t* h_draft_len, const float* d_q, const int32_t* d_probe_ids, int32_t n_probe,
+                      const rv_fusion* fusion, uint64_t seed, bool sampled, int32_t* d_accept_len,
+                      int32_t* d_next_id, void* stream) {
   if (!c || !h_prefix_len || !fusion || !d_accept_len || !d_next_id)
     return fail(RV_E_ARG, "cache, prefix_len, fusion and outputs must not be NULL");
   if (sampled != (fusion->rule == RV_RULE_SAMPLING))
@@ -782,18 +789,25 @@ rv_status verify_impl(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d
       return fail(RV_E_ARG, "unknown entropy source %d", fusion->entropy_src);
   }
   const int P = fusion->prefix_pos;
-  const long long S = 1LL + 2LL * k + n_probe + P;
-  if (S > c->max_block) return fail(RV_E_CAPACITY, "block of %lld rows exceeds max_block=%d", S, c->max_block);
-  int kmax = 0;
+  uint8_t kb[RV_MAX_BATCH];
+  int S_max = 0, M = 0, R1 = 0, kmax = 0;
   for (int b = 0; b < c->B; ++b) {
+    const int kk = h_draft_len ? h_draft_len[b] : k;
+    if (kk < 0 || kk > k) return fail(RV_E_ARG, "draft count %d of sequence %d outside [0, %d]", kk, b, k);
+    kb[b] = (uint8_t)kk;
+    const long long S = 1LL + 2LL * kk + n_probe + P;
+    if (S > c->max_block) return fail(RV_E_CAPACITY, "block of %lld rows exceeds max_block=%d", S, c->max_block);
     const int L = h_prefix_len[b];
     if (L < std::max(1, P) || L > c->max_len)
       return fail(RV_E_RANGE, "prefix_len[%d] = %d outside [max(1, P)=%d, max_len=%d]", b, L, std::max(1, P),
                   c->max_len);
-    if ((long long)L - 1 + S > c->max_len || (long long)L + k + 1 > c->max_len)
+    if ((long long)L - 1 + S > c->max_len || (long long)L + kk + 1 > c->max_len)
       return fail(RV_E_CAPACITY, "sequence %d: block of %lld rows at length %d exceeds max_len=%d", b, S, L,
                   c->max_len);
     kmax = std::max(kmax, (int)(L - 1 + S));
+    S_max = std::max(S_max, (int)S);
+    M += (int)S;
+    R1 += kk + 1;
   }
   hipStream_t st = (hipStream_t)stream;
   rv_model* m = c->m;
@@ -802,8 +816,10 @@ rv_status verify_impl(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d
 
   PlanVerify pv{};
   pv.B = c->B;
-  pv.S = (int)S;
+  pv.S = S_max;
   pv.k = k;
+  pv.lm_src = c->lm_src;
+  for (int b = 0; b < c->B; ++b) pv.kb[b] = kb[b];
   pv.n_probe = n_probe;
   pv.P = P;
   pv.d = mc.d_model;
@@ -827,17 +843,15 @@ rv_status verify_impl(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d
     HIP_TRY(launch_plan_verify(dt, pv, st), "verify plan");
   }
 
-  const int M = c->B * (int)S;
   int pending = 0;
-  rv_status s = run_layers(c, M, c->B, (int)S, kmax, true, &pending, st);
+  rv_status s = run_layers(c, M, c->B, S_max, kmax, true, &pending, st);
   if (s != RV_OK) return s;
 
-  // LM head on the 2(k+1) rows per sequence that Algorithm 1 reads.
-  const int shift = k + n_probe + P;
-  const int nout = c->B * 2 * (k + 1);
+  // LM head on the 2(k_b+1) rows per sequence that Algorithm 1 reads.
+  const int nout = 2 * R1;
   {
     Prof pf(c, RV_PROF_NORM, st);
-    HIP_TRY(launch_rmsnorm(dt, c->h, nout, mc.d_model, m->norm_f, mc.rms_eps, c->lm_x, c->lm_x2, (int)S, k, shift,
+    HIP_TRY(launch_rmsnorm(dt, c->h, nout, mc.d_model, m->norm_f, mc.rms_eps, c->lm_x, c->lm_x2, c->lm_src,
                            pending > 1 ? c->gpart : nullptr, pending, M, st),
             "final norm");
   }
@@ -859,7 +873,10 @@ rv_status verify_impl(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d
   ha.B = c->B;
   ha.k = k;
   ha.V = mc.vocab;
-  ha.S = (int)S;
+  ha.n_probe = n_probe;
+  ha.P = P;
+  ha.R1 = R1;
+  for (int b = 0; b < c->B; ++b) ha.kb[b] = kb[b];
   ha.max_len = c->max_len;
   ha.nchunk = c->nchunk;
   ha.chunk = kVocabChunk;
@@ -891,6 +908,8 @@ rv_status verify_impl(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d
     HIP_TRY(launch_head(ha, st), "accept");
   }
   c->last_k = k;
+  c->last_R1 = R1;
+  for (int b = 0; b < c->B; ++b) c->last_kb[b] = kb[b];
   return RV_OK;
 }
 
@@ -901,16 +920,24 @@ extern "C" {
 rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t k,
                     const int32_t* d_probe_ids, int32_t n_probe, const rv_fusion* fusion, int32_t* d_accept_len,
                     int32_t* d_next_id, void* stream) {
-  return verify_impl(c, h_prefix_len, d_draft_ids, k, nullptr, d_probe_ids, n_probe, fusion, 0, false,
+  return verify_impl(c, h_prefix_len, d_draft_ids, k, nullptr, nullptr, d_probe_ids, n_probe, fusion, 0, false,
                      d_accept_len, d_next_id, stream);
+}
+
+rv_status rv_verify_ragged(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t ld_drafts,
+                           const int32_t* h_draft_len, const int32_t* d_probe_ids, int32_t n_probe,
+                           const rv_fusion* fusion, int32_t* d_accept_len, int32_t* d_next_id, void* stream) {
+  if (!h_draft_len) return fail(RV_E_ARG, "draft lengths must not be NULL");
+  return verify_impl(c, h_prefix_len, d_draft_ids, ld_drafts, h_draft_len, nullptr, d_probe_ids, n_probe, fusion, 0,
+                     false, d_accept_len, d_next_id, stream);
 }
 
 rv_status rv_verify_sampled(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t k,
                             const float* d_draft_probs, const int32_t* d_probe_ids, int32_t n_probe,
                             const rv_fusion* fusion, uint64_t seed, int32_t* d_accept_len,
                             int32_t* d_next_id, void* stream) {
-  return verify_impl(c, h_prefix_len, d_draft_ids, k, d_draft_probs, d_probe_ids, n_probe, fusion, seed, true,
-                     d_accept_len, d_next_id, stream);
+  return verify_impl(c, h_prefix_len, d_draft_ids, k, nullptr, d_draft_probs, d_probe_ids, n_probe, fusion, seed,
+                     true, d_accept_len, d_next_id, stream);
 }
 
 rv_status rv_debug_output(const rv_cache* c, int32_t which, float* d_dst, size_t dst_bytes, void* stream) {
@@ -920,24 +947,29 @@ rv_status rv_debug_output(const rv_cache* c, int32_t which, float* d_dst, size_t
   const int k1 = c->last_k + 1;
   hipStream_t st = (hipStream_t)stream;
   if (which == RV_OUT_ENTROPY || which == RV_OUT_MARGINS) {
-    const size_t n = which == RV_OUT_ENTROPY ? (size_t)2 * c->B * k1 : (size_t)c->B * (k1 + 1);
+    const size_t n = which == RV_OUT_ENTROPY ? (size_t)2 * c->last_R1 : (size_t)c->B * (k1 + 1);
     if (dst_bytes < n * 4) return fail(RV_E_BUFFER, "destination needs %zu bytes", n * 4);
     HIP_TRY(hipMemcpyAsync(d_dst, which == RV_OUT_ENTROPY ? c->entropy : c->margins, n * 4,
                            hipMemcpyDeviceToDevice, st),
             "copy");
     return RV_OK;
   }
-  const size_t V = c->m->cfg.vocab, row_bytes = (size_t)k1 * V * 4;
-  if (dst_bytes < row_bytes * c->B) return fail(RV_E_BUFFER, "destination needs %zu bytes", row_bytes * c->B);
+  const size_t V = c->m->cfg.vocab, R1 = c->last_R1, bytes = R1 * V * 4;
+  if (dst_bytes < bytes) return fail(RV_E_BUFFER, "destination needs %zu bytes", bytes);
   if (which == RV_OUT_ORIG || which == RV_OUT_REFL) {
-    const float* src = c->logits + (which == RV_OUT_REFL ? (size_t)k1 * V : 0);
-    HIP_TRY(hipMemcpy2DAsync(d_dst, row_bytes, src, 2 * row_bytes, row_bytes, c->B, hipMemcpyDeviceToDevice, st),
-            "copy");
+    // sequence b: logit rows 2 (b + K_b) .. (o rows, then r rows), fused rows b + K_b ..
+    size_t zrow = 0;
+    for (int b = 0; b < c->B; ++b) {
+      const size_t kb1 = (size_t)c->last_kb[b] + 1;
+      const float* src = c->logits + (2 * zrow + (which == RV_OUT_REFL ? kb1 : 0)) * V;
+      HIP_TRY(hipMemcpyAsync(d_dst + zrow * V, src, kb1 * V * 4, hipMemcpyDeviceToDevice, st), "copy");
+      zrow += kb1;
+    }
   } else if (which == RV_OUT_FUSED) {
-    HIP_TRY(hipMemcpyAsync(d_dst, c->z, row_bytes * c->B, hipMemcpyDeviceToDevice, st), "copy");
+    HIP_TRY(hipMemcpyAsync(d_dst, c->z, bytes, hipMemcpyDeviceToDevice, st), "copy");
   } else {
     const size_t f = which - RV_OUT_LOGP_ORIG;
-    HIP_TRY(hipMemcpyAsync(d_dst, c->lp + f * c->B * k1 * V, row_bytes * c->B, hipMemcpyDeviceToDevice, st), "copy");
+    HIP_TRY(hipMemcpyAsync(d_dst, c->lp + f * R1 * V, bytes, hipMemcpyDeviceToDevice, st), "copy");
   }
   return RV_OK;
 }

@@ -93,15 +93,22 @@ hipError_t launch_attention(int dtype, const AttnArgs& a, int n_qgroups, hipStre
 hipError_t launch_attn_combine(int dtype, const AttnArgs& a, hipStream_t st);
 
 // ---------------------------------------------------------------- norms and planning
-// RMSNorm of rows of the fp32 residual h into matmul operands (out, out2).  With gather_k >= 0
-// the output row r = b * 2(k+1) + j reads source row b*S + j (j <= k) or
-// b*S + shift + j - (k+1) (the rows the LM head needs).
+// RMSNorm of rows of the fp32 residual h into matmul operands (out, out2).  Output row r
+// reads source row gather[r] (gather != NULL: the rows the LM head needs) or r.
 // With P != NULL the source row first takes h += sum over g < gk of P[g][row]
 // (k-group order; P holds p_rows rows per k-group) and writes h back (the
 // pending partials of the previous matmul).
 hipError_t launch_rmsnorm(int dtype, float* h, int rows, int d, const float* gain, float eps, void* out,
-                          void* out2, int gather_S, int gather_k, int gather_shift, const float* P, int gk,
-                          int p_rows, hipStream_t st);
+                          void* out2, const int* gather, const float* P, int gk, int p_rows, hipStream_t st);
+
+// Per-sequence draft counts k_b of a verify pass (uniform passes have k_b = k).
+// Block b has S_b = 1 + 2 k_b + n_probe + P rows from row b (1 + n_probe + P)
+// + 2 K_b, and k_b + 1 fused rows from row b + K_b, with K_b = sum_{b' < b} k_b'.
+RV_DEV inline int kb_prefix(const uint8_t* kb, int b) {
+  int s = 0;
+  for (int i = 0; i < b; ++i) s += kb[i];
+  return s;
+}
 
 struct QkvFinish {
   const float* P;        // [gk][M][N] partials of the packed QKV matrix (physical rows)
@@ -124,9 +131,10 @@ hipError_t launch_qkv_finish(int dtype, const QkvFinish& a, hipStream_t st);
 hipError_t launch_retile(int dtype, const void* src, void* dst, int rows, int K, bool to_tiles, hipStream_t st);
 
 struct PlanVerify {
-  int B, S, k, n_probe, P, d, V, max_len;
+  int B, S, k, n_probe, P, d, V, max_len;  // S: largest block, k: draft-id stride
   const int* ids;        // history [B][max_len]
-  const int* drafts;     // [B][k]
+  const int* drafts;     // [B][k], sequence b uses the first kb[b]
+  int* lm_src;           // [sum 2(k_b+1)]: block row feeding each LM-head row
   const int* probe;      // [n_probe]
   const void* embed;     // [V][d] T
   float* h;              // [rows][d]
@@ -138,6 +146,7 @@ struct PlanVerify {
   int* seg_n;
   int* seg_pos0;
   int L[RV_MAX_BATCH];
+  uint8_t kb[RV_MAX_BATCH];
 };
 hipError_t launch_plan_verify(int dtype, const PlanVerify& p, hipStream_t st);
 
@@ -168,7 +177,8 @@ hipError_t launch_store_ids(const StoreIds& s, hipStream_t st);
 
 // ---------------------------------------------------------------- LM-head tail
 struct HeadArgs {
-  int B, k, V, S, max_len, nchunk, chunk;
+  int B, k, V, max_len, nchunk, chunk;  // k: largest draft count (draft-id and margin stride k + 2)
+  int n_probe, P, R1;                   // R1 = sum (k_b + 1) fused rows
   float alpha;
   int rule;              // RV_RULE_GREEDY / RV_RULE_TYPICAL
   float eps, delta;      // typical threshold parameters
@@ -176,20 +186,21 @@ struct HeadArgs {
   float temp;            // fused logits are divided by it (1: unchanged)
   const float* q;        // sampling: draft distributions [B][k][V]
   uint64_t seed;         // sampling: Philox key word 0
-  const float* logits;   // [B][2(k+1)][V]: o rows then r rows per sequence
-  float* z;              // [B][k+1][V]
-  float* part;           // [4][B*(k+1)][nchunk][4]: (max, sum, centred sum) of o, r, z; z's top-2
-  float* lse;            // [3][B*(k+1)]
-  float* entropy;        // [2][B*(k+1)]: entropy of softmax(z), then of softmax(o)
-  float* lp;             // [3][B][k+1][V]: log-softmax of o, r, z
-  float* margins;        // [B][k+2]: margins of tested drafts, then top1-top2 gap
+  const float* logits;   // per sequence 2(k_b+1) rows: o rows then r rows
+  float* z;              // [R1][V], sequence b from row b + K_b
+  float* part;           // [4][R1][nchunk][4]: (max, sum, centred sum) of o, r, z; z's top-2
+  float* lse;            // [3][R1]
+  float* entropy;        // [2][R1]: entropy of softmax(z), then of softmax(o)
+  float* lp;             // [3][R1][V]: log-softmax of o, r, z
+  float* margins;        // [B][k+2]: margins of tested drafts, then top1-top2 gap last
   const int* drafts;     // [B][k]
   int* ids;              // history [B][max_len]
-  const int* row_bad;    // [B*S]
+  const int* row_bad;    // [block rows]
   const int* seq_bad;    // [B]
   int* accept_len;
   int* next_id;
-  int* argmax;           // [B][k+1]
+  int* argmax;           // [R1]
   int L[RV_MAX_BATCH];
+  uint8_t kb[RV_MAX_BATCH];
 };
 hipError_t launch_head(const HeadArgs& a, hipStream_t st);

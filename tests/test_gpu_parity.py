@@ -337,3 +337,67 @@ def test_validation_errors_enqueue_nothing(rv, gpu):
     assert code() == "RV_OK"
     torch.cuda.synchronize()
     v.close()
+
+
+@pytest.mark.parametrize("shape", [workload.TINY, workload.TINY_GQA_BF16], ids=lambda s: s.name)
+@pytest.mark.parametrize("typical", [None, (0.09, 0.3, "fused")])
+def test_ragged_draft_counts_match_oracle(rv, gpu, shape, typical):
+    """A draft count per sequence (dynamic draft length): each sequence gets
+    what the oracle computes for its own block."""
+    import torch
+    kl = [0, 3, 5, 1]
+    hists = [workload.random_ids(shape.vocab, L, 9, b) for b, L in enumerate([44, 70, 52, 61])]
+    drafts = [draft_case(shape, 2, h, k, 0.3, 90 + b) if k else [] for b, (h, k) in enumerate(zip(hists, kl))]
+    probe = workload.random_ids(shape.vocab, 6, 9, 0xBEEF)
+    P, alpha = 4, 0.3
+    S = 1 + 2 * max(kl) + len(probe) + P
+    v = rv.Verifier(shape, 2, len(hists), max(len(h) for h in hists) + S + 8, max_block=S, max_drafts=max(kl))
+    lens = v.prefill([list(map(int, h)) for h in hists])
+    kw = {}
+    if typical:
+        kw = dict(rule=rv.RV_RULE_TYPICAL, epsilon=typical[0], delta=typical[1])
+    acc, nxt = v.verify_ragged(lens, drafts, probe, alpha, P, **kw)
+    torch.cuda.synchronize()
+    acc, nxt = acc.cpu().numpy().copy(), nxt.cpu().numpy().copy()
+    out = {w: v.output(w).cpu().numpy() for w in range(8)}
+    row = 0
+    for b in range(len(hists)):
+        okw = dict(rule="typical", eps=typical[0], delta=typical[1], entropy_of=typical[2]) if typical else {}
+        ref = oracle.verify(shape, 2, list(map(int, hists[b])), drafts[b], probe, alpha, P, **okw)
+        rows = slice(row, row + kl[b] + 1)
+        logits_close(shape, out[rv.RV_OUT_ORIG][rows], ref["o"])
+        logits_close(shape, out[rv.RV_OUT_REFL][rows], ref["r"])
+        logits_close(shape, out[rv.RV_OUT_FUSED][rows], ref["z"])
+        s = np.exp(out[rv.RV_OUT_LOGP_FUSED][rows].astype(np.float64)).sum(-1)
+        assert np.abs(s - 1).max() < 1e-4
+        h_tol = 5e-4 if shape.dtype == "f32" else 2e-2 * max(1.0, float(np.abs(ref["h_z"]).max()))
+        assert np.abs(out[rv.RV_OUT_ENTROPY][0][rows] - ref["h_z"]).max() < h_tol
+        if not ref["near_tie"]:
+            assert (int(acc[b]), int(nxt[b])) == (ref["accept_len"], ref["next_id"]), (b, ref["margins"])
+        # history: prefix + accepted drafts + t
+        n = int(acc[b])
+        ids = torch.empty(lens[b] + n + 1, dtype=torch.int32, device="cuda")
+        rv.rv_debug_export_ids(v.cache, b, 0, lens[b] + n + 1, ids)
+        torch.cuda.synchronize()
+        assert ids.cpu().tolist() == list(map(int, hists[b])) + list(drafts[b][:n]) + [int(nxt[b])]
+        row += kl[b] + 1
+    v.close()
+
+
+def test_ragged_with_equal_counts_is_the_uniform_call(rv, gpu):
+    import torch
+    shape = workload.TINY_GQA_BF16
+    hists = [workload.random_ids(shape.vocab, L, 10, b) for b, L in enumerate([40, 57])]
+    drafts = [draft_case(shape, 1, h, 3, 0.3, 100 + b) for b, h in enumerate(hists)]
+    probe = workload.random_ids(shape.vocab, 4, 10, 0xBEEF)
+    v = rv.Verifier(shape, 1, 2, 100, max_block=16, max_drafts=3)
+    lens = v.prefill([list(map(int, h)) for h in hists])
+    a1, n1 = v.verify(lens, np.array(drafts), probe, 0.3, 4)
+    torch.cuda.synchronize()
+    r1 = (a1.cpu().numpy().copy(), n1.cpu().numpy().copy(), {w: v.output(w).cpu().numpy() for w in range(8)})
+    a2, n2 = v.verify_ragged(lens, drafts, probe, 0.3, 4)
+    torch.cuda.synchronize()
+    assert (a2.cpu().numpy() == r1[0]).all() and (n2.cpu().numpy() == r1[1]).all()
+    for w in range(6):
+        np.testing.assert_array_equal(v.output(w).cpu().numpy().reshape(r1[2][w].shape), r1[2][w])
+    v.close()
