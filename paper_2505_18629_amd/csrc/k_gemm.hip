@@ -320,7 +320,7 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm_tiled(GemmArgs a, int n_rk
 
 template <int DT, int NT, int MTT, int EPI>
 void launch_one(const GemmArgs& a, unsigned items, hipStream_t st) {
-  constexpr int kDepth = NT == 8 ? 2 : 4;
+  constexpr int kDepth = NT >= 6 ? 2 : 4;
   const dim3 block(kWaves * 64);
   LaunchEvents& ev = g_launch_events;
   if (ev.start) {
@@ -357,6 +357,12 @@ hipError_t launch_epi(const GemmArgs& a, int nt, int mtt, hipStream_t st) {
     case 2: return launch_nt<DT, 2, EPI>(a, mtt, st);
     case 4: return launch_nt<DT, 4, EPI>(a, mtt, st);
     case 8: return launch_nt<DT, 8, EPI>(a, mtt, st);
+    case 3:
+    case 6:
+      // only K-split launches use 3 or 6 row tiles
+      if constexpr (EPI == EPI_PARTIAL) return nt == 3 ? launch_nt<DT, 3, EPI>(a, mtt, st)
+                                                       : launch_nt<DT, 6, EPI>(a, mtt, st);
+      break;
   }
   return hipErrorInvalidValue;
 }

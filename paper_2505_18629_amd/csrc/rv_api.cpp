@@ -327,6 +327,22 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K, bool allow_split, in
   // ~200 workgroups already saturate HBM (8B gate/up: 5.1 -> 6.0 TB/s).
   const bool wide = dtype == RV_BF16 && p.mtt == 2 && (long long)N * K >= (32LL << 20) && N % 128 == 0;
   if (allow_split && M <= kSplitRows && N % 64 == 0) {
+    // Prefer a launch of exactly one workgroup per CU (measured at the 8B
+    // shapes: down 8 tiles x 8 k-groups 22.6 -> 21.4 us, QKV 6 x 4
+    // 12.8 -> 11.1 us, O 4 x 4 8.3 -> 8.1 us).
+    const int nts[] = {8, 6, 4, 3, 2};
+    const int cand1[] = {2, 4, 7, 8, 14, 16};
+    for (int nt : nts) {
+      if ((nt == 8 && !wide) || (nt > 4 && p.mtt > 2) || N % (16 * nt)) continue;
+      for (int gk : cand1) {
+        if (ksteps % (4 * gk) || gk * M > part_rows) continue;
+        if ((long long)(N / (16 * nt)) * gk * p.n_tg == 256) {
+          p.nt = nt;
+          p.gk = gk;
+          return p;
+        }
+      }
+    }
     p.nt = wide ? 8 : 4;
     const int target = wide ? kTarget / 2 : kTarget;
     const int cand[] = {1, 2, 4, 7, 8, 14, 16};
