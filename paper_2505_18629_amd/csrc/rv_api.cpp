@@ -455,7 +455,10 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, b
     g.k_rows = m->qkv.k_rows;
     {
       // few-row passes split K; the partials are finished (sum, rotary,
-      // q operand and KV writes) by a small per-token kernel
+      // q operand and KV writes) by a small per-token kernel.  (Finishing
+      // them in the last-arriving k-group workgroup instead needs an
+      // agent-scope release per workgroup, an L2 writeback each: measured
+      // slower than the extra launch.)
       Prof pf(c, RV_PROF_QKV, st);
       const GemmPlan qp = plan_gemm(dt, EPI_RESID, M, g.N, g.K, true, c->gpart_rows);
       if (qp.gk > 1) {
