@@ -181,51 +181,49 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
         }
       }
 
-    // online softmax (log2 units).  Interior tiles (every key valid and at
-    // or before the earliest query of this workgroup) need no mask; the
-    // first tile needs no rescale of the zero accumulators.
+    // online softmax in log2 units: p = 2^(s*scale - m), m the running
+    // maximum of the scaled scores (scaling by a positive constant keeps the
+    // argmax, so the raw maximum is scaled once).  Interior tiles (every key
+    // valid and at or before the earliest query of this workgroup) need no
+    // mask; the first tile needs no rescale of the zero accumulators.
     const bool interior = kt0 + kKB <= kend && kt0 + kKB - 1 <= qpos_min;
     const bool first = kt0 == kbeg;
+    const float c = a.scale_log2;
 #pragma unroll
     for (int t = 0; t < TPW; ++t) {
-      float mloc = -INFINITY;
-      if (interior) {
-#pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            s[t][kt][i] *= a.scale_log2;
-            mloc = fmaxf(mloc, s[t][kt][i]);
-          }
-      } else {
+      if (!interior) {
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int key = kt0 + 16 * kt + 4 * g + i;
-            const bool ok = key < kend && key <= qpos[t];
-            s[t][kt][i] = ok ? s[t][kt][i] * a.scale_log2 : -INFINITY;
-            mloc = fmaxf(mloc, s[t][kt][i]);
+            if (!(key < kend && key <= qpos[t])) s[t][kt][i] = -INFINITY;
           }
       }
+      float mloc = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) mloc = fmaxf(mloc, fmaxf(fmaxf(s[t][kt][0], s[t][kt][1]), fmaxf(s[t][kt][2], s[t][kt][3])));
       mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
       mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      const float m_new = fmaxf(m_run[t], mloc);
+      const float m_new = fmaxf(m_run[t], mloc * c);
       const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float rescale = exp2f(m_run[t] - m_use);
+      const float rescale = __builtin_amdgcn_exp2f(m_run[t] - m_use);
       float psum = 0.f;
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          s[t][kt][i] = exp2f(s[t][kt][i] - m_use);
+          s[t][kt][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][kt][i], c, -m_use));
           psum += s[t][kt][i];
         }
       psum += __shfl_xor(psum, 16, 64);
       psum += __shfl_xor(psum, 32, 64);
       l_run[t] = l_run[t] * rescale + psum;
+      // rescale is exactly 1 where the maximum did not grow: the wave skips
+      // the multiply when that holds for all its lanes
+      const bool grew = m_new != m_run[t];
       m_run[t] = m_new;
-      if (!first) {
+      if (!first && __any(grew)) {
 #pragma unroll
         for (int d = 0; d < DT; ++d) O[t][d] *= rescale;
       }

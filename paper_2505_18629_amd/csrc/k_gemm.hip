@@ -231,18 +231,14 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm_tiled(GemmArgs a, int n_rk
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int ksteps = a.K / 32;
-  // Item = (row group, k-group) x token group, in an XCD-aware order
-  // (workgroup b runs on XCD b % 8).
+  // Item = (row group, k-group) x token group, in an XCD-aware order:
+  // workgroup b runs on XCD b % 8, and the n_tg workgroups of one (row group,
+  // k-group) share that XCD.  The grid covers n_rk rounded up to a multiple
+  // of 8; the workgroups past n_rk have no item.
   const int b = blockIdx.x;
-  int rk, tg;
-  if (n_rk % 8 == 0) {
-    const int j = b / 8;
-    rk = (j / a.n_tg) * 8 + b % 8;
-    tg = j % a.n_tg;
-  } else {
-    rk = b / a.n_tg;
-    tg = b % a.n_tg;
-  }
+  const int j = b / 8;
+  const int rk = (j / a.n_tg) * 8 + b % 8, tg = j % a.n_tg;
+  if (rk >= n_rk) return;
   const int rg = rk / a.gk, kg = rk % a.gk;
   const int ks = ksteps / a.gk, kb = kg * ks;  // this k-group's steps
   const int tile0 = (rg * kWaves + w) * NT;    // this wave's first row tile
@@ -383,7 +379,7 @@ hipError_t launch_dt(int epi, const GemmArgs& a, int nt, int mtt, hipStream_t st
 template <int NT, int MT, int EPI>
 hipError_t launch_tiled_one(const GemmArgs& a, hipStream_t st) {
   const int n_rk = a.N / (16 * kWaves * NT) * a.gk;
-  const unsigned items = (unsigned)(n_rk * a.n_tg);
+  const unsigned items = (unsigned)((n_rk + 7) / 8 * 8 * a.n_tg);
   const dim3 block(kWaves * 64);
   LaunchEvents& ev = g_launch_events;
   if (ev.start) {
