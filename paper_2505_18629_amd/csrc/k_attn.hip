@@ -20,33 +20,34 @@ constexpr int kKB = 64;  // keys per LDS tile
 
 // ----------------------------------------------------------- bf16, MFMA
 //
-// S^T = K Q^T: A = K tile (16 keys x 32 d), B = Q^T (32 d x 16 queries), so
+// S^T = K Q^T: A = K unit (16 keys x 32 d), B = Q^T (32 d x 16 queries), so
 // lane l holds the scores of keys 4*(l/16)+i for query l%16.
-// O^T += V^T P^T: A = V^T (16 d x 32 keys), B = P^T taken directly from the
-// score registers: hardware k slot j of lane group g is key 4g+j (j < 4) of
-// the first 16-key tile of a 32-key chunk and key 16+4g+(j-4) of the second.
-// V^T is staged in LDS with its keys in that slot order, so each A operand
-// is one 16-byte LDS read.  Q, K, V and P are all (hi, lo) bf16 pairs; each
-// product is hi*hi + hi*lo + lo*hi (three MFMAs; lo*lo is ~2^-16 of the
-// result and dropped).
+// O^T += V^T P^T: A = V^T unit (16 d x 32 keys), B = P^T taken directly from
+// the score registers: hardware k slot j of lane group g is key 4g+j (j < 4)
+// of the first 16-key block of a 32-key chunk and key 16+4g+(j-4) of the
+// second, the slot order the V cache is stored in.  Q, K, V and P are all
+// (hi, lo) bf16 pairs; each product is hi*hi + hi*lo + lo*hi (three MFMAs;
+// lo*lo is ~2^-16 of the result and dropped).
 //
-// Every load is unconditional: rows past the valid range are clamped to a
-// valid row, and their results are masked (scores set to -inf, so their P
-// is exactly 0 against a finite V) or not stored.
+// The cache keeps K and V in operand order (put_k4 / put_v4), so a 64-key
+// tile is four contiguous spans (K hi, K lo, V hi, V lo) that the workgroup
+// copies global -> LDS with 16-byte direct loads, double-buffered: tile t+1
+// is in flight while tile t is multiplied, and every MFMA operand is one
+// conflict-free 16-byte LDS read per lane.  Tiles are 64-aligned and the
+// cache holds whole tiles, so copies need no clamping; keys past the valid
+// range hold finite values (the cache starts zeroed) and are masked (score
+// -inf, so P is exactly 0) or belong to queries whose results are not stored.
 template <int HD, int NW, int TPW>
 __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
   static_assert(NW * TPW == 8, "a workgroup covers 128 queries");
-  constexpr int NTH = NW * 64;
-  constexpr int KSTR = HD + 8;     // padded K row (elements)
-  constexpr int VSTR = kKB + 8;    // padded V^T row (elements)
-  constexpr int DC = HD / 32;      // d chunks for QK^T
-  constexpr int DT = HD / 16;      // d tiles for PV
-  constexpr int KCH = kKB * HD / 8;            // 16-byte K chunks per tile
-  constexpr int KPER = KCH >= NTH ? KCH / NTH : 1;  // per thread
-  static_assert(KCH % NTH == 0 || NTH % KCH == 0, "K chunks must tile the workgroup");
-  constexpr int VCOMB = 2 * 4 * (HD / 4);      // (chunk, lane group, 4-d group) V units
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kKB * KSTR];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][HD * VSTR];
+  constexpr int DC = HD / 32;                 // d chunks for QK^T
+  constexpr int DT = HD / 16;                 // d tiles for PV
+  constexpr int SPAN = kKB * HD;              // elements of one plane of a tile
+  constexpr int UNITS = 4 * SPAN / 512;       // 1 KiB units per tile (4 spans)
+  constexpr int UPW = UNITS / NW;             // units each wave copies
+  static_assert(UNITS % NW == 0, "tile units must divide among the waves");
+  __shared__ __attribute__((aligned(16))) uint16_t sm0[4][SPAN];
+  __shared__ __attribute__((aligned(16))) uint16_t sm1[4][SPAN];
 
   const int split = blockIdx.x, qg = blockIdx.y, grp = blockIdx.z;
   const int seg = grp / a.n_kv, kvh = grp % a.n_kv;
@@ -60,13 +61,28 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
   const int kbeg = split * a.ks, kend = min(kmax, kbeg + a.ks);
   const int qpos_min = pos0 + q_begin / G;
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int qd = a.n_heads * HD;
-  const size_t kvoff = (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
-  const uint16_t* kbase0 = (const uint16_t*)a.kc + kvoff;
-  const uint16_t* kbase1 = (const uint16_t*)a.kc2 + kvoff;
-  const uint16_t* vbase0 = (const uint16_t*)a.vc + kvoff;
-  const uint16_t* vbase1 = (const uint16_t*)a.vc2 + kvoff;
+  const size_t kvoff = (size_t)(b * a.n_kv + kvh) * a.kv_len * HD;
+
+  // the spans this wave copies: unit u of the tile is span u / (UNITS/4)
+  const uint16_t* src[UPW];
+  int dst[UPW];
+#pragma unroll
+  for (int i = 0; i < UPW; ++i) {
+    const int u = w * UPW + i, sp = u / (UNITS / 4), off = (u % (UNITS / 4)) * 512;
+    const void* base = sp == 0 ? a.kc : sp == 1 ? a.kc2 : sp == 2 ? a.vc : a.vc2;
+    src[i] = (const uint16_t*)base + kvoff + off + lane * 8;
+    dst[i] = sp * SPAN + off;
+  }
+  auto fetch = [&](uint16_t(&sm)[4][SPAN], int kt0) {
+#pragma unroll
+    for (int i = 0; i < UPW; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(src[i] + (size_t)kt0 * HD),
+                                       (__attribute__((address_space(3))) void*)(&sm[0][0] + dst[i]), 16, 0, 0);
+  };
+  if (kbeg < kend) fetch(sm0, kbeg);
 
   // Queries of this wave: TPW 16-query tiles, hi and lo operand planes.
   uint4 qB[2][TPW][DC];
@@ -99,66 +115,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
 #pragma unroll
     for (int d = 0; d < DT; ++d) O[t][d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // Tile staging through registers (the next tile's loads are in flight
-  // while the current one is computed).  K: thread chunk u is key c/(HD/8),
-  // dims 8*(c%(HD/8)).  V: thread unit (chunk vc, lane group vg, dims
-  // 4*vd..4*vd+3) loads the 8 keys of that slot group, 4 dims each, and
-  // writes them transposed as 4 rows of 8 slot-ordered keys.
-  const bool kthr = KCH >= NTH || tid < KCH;  // wave-uniform (KCH is a multiple of 64)
-  const bool vthr = tid < VCOMB;
-  const int vc = tid / (4 * (HD / 4)), vg = (tid / (HD / 4)) % 4, vd = tid % (HD / 4);
-  u32x4 kr[2][KPER];
-  uint2 vr[2][8];
-#define RV_ATTN_FETCH(KT0)                                                                         \
-  do {                                                                                             \
-    if (kthr) {                                                                                    \
-      _Pragma("unroll") for (int u = 0; u < KPER; ++u) {                                           \
-        const int c_ = tid + u * NTH;                                                              \
-        const int key_ = min((KT0) + c_ / (HD / 8), kend - 1), d0_ = (c_ % (HD / 8)) * 8;          \
-        kr[0][u] = *(const u32x4*)(kbase0 + (size_t)key_ * HD + d0_);                              \
-        kr[1][u] = *(const u32x4*)(kbase1 + (size_t)key_ * HD + d0_);                              \
-      }                                                                                            \
-    }                                                                                              \
-    if (vthr) {                                                                                    \
-      _Pragma("unroll") for (int j = 0; j < 8; ++j) {                                              \
-        const int key_ = min((KT0) + 32 * vc + (j < 4 ? 4 * vg + j : 16 + 4 * vg + j - 4), kend - 1); \
-        vr[0][j] = *(const uint2*)(vbase0 + (size_t)key_ * HD + 4 * vd);                           \
-        vr[1][j] = *(const uint2*)(vbase1 + (size_t)key_ * HD + 4 * vd);                           \
-      }                                                                                            \
-    }                                                                                              \
-  } while (0)
-  if (kbeg < kend) RV_ATTN_FETCH(kbeg);
-  for (int kt0 = kbeg; kt0 < kend; kt0 += kKB) {
-    __syncthreads();
-    if (kthr) {
-#pragma unroll
-      for (int u = 0; u < KPER; ++u) {
-        const int c = tid + u * NTH;
-        const int kk = c / (HD / 8), d0 = (c % (HD / 8)) * 8;
-        *(u32x4*)(sK[0] + kk * KSTR + d0) = kr[0][u];
-        *(u32x4*)(sK[1] + kk * KSTR + d0) = kr[1][u];
-      }
-    }
-    if (vthr) {
-#pragma unroll
-      for (int pl = 0; pl < 2; ++pl)
-#pragma unroll
-        for (int dd = 0; dd < 4; ++dd) {
-          // element dd of each key's 4 dims: low or high half of word dd/2
-          uint32_t wv[4];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const uint32_t e0 = dd < 2 ? vr[pl][2 * j].x : vr[pl][2 * j].y;
-            const uint32_t e1 = dd < 2 ? vr[pl][2 * j + 1].x : vr[pl][2 * j + 1].y;
-            wv[j] = (dd & 1) ? ((e0 >> 16) | (e1 & 0xffff0000u)) : ((e0 & 0xffffu) | (e1 << 16));
-          }
-          *(uint4*)(sV[pl] + (4 * vd + dd) * VSTR + 32 * vc + 8 * vg) = uint4{wv[0], wv[1], wv[2], wv[3]};
-        }
-    }
-    __syncthreads();
-    if (kt0 + kKB < kend) RV_ATTN_FETCH(kt0 + kKB);
-
-    // scores for 64 keys x 2 query tiles
+  // One 64-key tile from the LDS buffer sm.
+  auto tile = [&](const uint16_t(&sm)[4][SPAN], int kt0) {
+    // scores for 64 keys x TPW query tiles
     f32x4_t s[TPW][4];
 #pragma unroll
     for (int t = 0; t < TPW; ++t)
@@ -168,9 +127,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
     for (int c = 0; c < DC; ++c)
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
-        const int ko = (16 * kt + (lane & 15)) * KSTR + 32 * c + g * 8;
-        const bf16x8_t kh = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK[0] + ko));
-        const bf16x8_t kl = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sK[1] + ko));
+        const int ko = (kt * DC + c) * 512 + lane * 8;
+        const bf16x8_t kh = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[0][ko]));
+        const bf16x8_t kl = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[1][ko]));
 #pragma unroll
         for (int t = 0; t < TPW; ++t) {
           const bf16x8_t qh = __builtin_bit_cast(bf16x8_t, qB[0][t][c]);
@@ -181,53 +140,53 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
         }
       }
 
-    // online softmax in log2 units: p = 2^(s*scale - m), m the running
-    // maximum of the scaled scores (scaling by a positive constant keeps the
-    // argmax, so the raw maximum is scaled once).  Interior tiles (every key
-    // valid and at or before the earliest query of this workgroup) need no
-    // mask; the first tile needs no rescale of the zero accumulators.
-    const bool interior = kt0 + kKB <= kend && kt0 + kKB - 1 <= qpos_min;
-    const bool first = kt0 == kbeg;
-    const float c = a.scale_log2;
+      // online softmax in log2 units: p = 2^(s*scale - m), m the running
+      // maximum of the scaled scores (scaling by a positive constant keeps the
+      // argmax, so the raw maximum is scaled once).  Interior tiles (every key
+      // valid and at or before the earliest query of this workgroup) need no
+      // mask; the first tile needs no rescale of the zero accumulators.
+      const bool interior = kt0 + kKB <= kend && kt0 + kKB - 1 <= qpos_min;
+      const bool first = kt0 == kbeg;
+      const float sc = a.scale_log2;
 #pragma unroll
-    for (int t = 0; t < TPW; ++t) {
-      if (!interior) {
+      for (int t = 0; t < TPW; ++t) {
+        if (!interior) {
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int key = kt0 + 16 * kt + 4 * g + i;
+              if (!(key < kend && key <= qpos[t])) s[t][kt][i] = -INFINITY;
+            }
+        }
+        float mloc = -INFINITY;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) mloc = fmaxf(mloc, fmaxf(fmaxf(s[t][kt][0], s[t][kt][1]), fmaxf(s[t][kt][2], s[t][kt][3])));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+        const float m_new = fmaxf(m_run[t], mloc * sc);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float rescale = __builtin_amdgcn_exp2f(m_run[t] - m_use);
+        float psum = 0.f;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int key = kt0 + 16 * kt + 4 * g + i;
-            if (!(key < kend && key <= qpos[t])) s[t][kt][i] = -INFINITY;
+            s[t][kt][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][kt][i], sc, -m_use));
+            psum += s[t][kt][i];
           }
-      }
-      float mloc = -INFINITY;
+        psum += __shfl_xor(psum, 16, 64);
+        psum += __shfl_xor(psum, 32, 64);
+        l_run[t] = l_run[t] * rescale + psum;
+        // rescale is exactly 1 where the maximum did not grow: the wave skips
+        // the multiply when that holds for all its lanes
+        const bool grew = m_new != m_run[t];
+        m_run[t] = m_new;
+        if (!first && __any(grew)) {
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt) mloc = fmaxf(mloc, fmaxf(fmaxf(s[t][kt][0], s[t][kt][1]), fmaxf(s[t][kt][2], s[t][kt][3])));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-      mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-      const float m_new = fmaxf(m_run[t], mloc * c);
-      const float m_use = m_new == -INFINITY ? 0.f : m_new;
-      const float rescale = __builtin_amdgcn_exp2f(m_run[t] - m_use);
-      float psum = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          s[t][kt][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][kt][i], c, -m_use));
-          psum += s[t][kt][i];
+          for (int d = 0; d < DT; ++d) O[t][d] *= rescale;
         }
-      psum += __shfl_xor(psum, 16, 64);
-      psum += __shfl_xor(psum, 32, 64);
-      l_run[t] = l_run[t] * rescale + psum;
-      // rescale is exactly 1 where the maximum did not grow: the wave skips
-      // the multiply when that holds for all its lanes
-      const bool grew = m_new != m_run[t];
-      m_run[t] = m_new;
-      if (!first && __any(grew)) {
-#pragma unroll
-        for (int d = 0; d < DT; ++d) O[t][d] *= rescale;
       }
-    }
 
     // O^T += V^T P^T with P split into hi/lo B operands
 #pragma unroll
@@ -245,17 +204,31 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
         }
 #pragma unroll
         for (int d = 0; d < DT; ++d) {
-          const int vo = (16 * d + (lane & 15)) * VSTR + 32 * c + 8 * g;
-          const bf16x8_t vh = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sV[0] + vo));
-          const bf16x8_t vl = __builtin_bit_cast(bf16x8_t, *(const uint4*)(sV[1] + vo));
+          const int vo = (c * DT + d) * 512 + lane * 8;
+          const bf16x8_t vh = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[2][vo]));
+          const bf16x8_t vl = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[3][vo]));
           O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh, phi, O[t][d], 0, 0, 0);
           O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh, plo, O[t][d], 0, 0, 0);
           O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vl, phi, O[t][d], 0, 0, 0);
         }
       }
-  }
+  };
 
-#undef RV_ATTN_FETCH
+  // Two tiles per iteration so each buffer is named statically.  At the top
+  // of each half only the copy of the tile about to be used is in flight;
+  // after the barrier every wave has finished the previous tile, so its
+  // buffer takes the next copy.
+  for (int kt0 = kbeg; kt0 < kend; kt0 += 2 * kKB) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (kt0 + kKB < kend) fetch(sm1, kt0 + kKB);
+    tile(sm0, kt0);
+    if (kt0 + kKB >= kend) break;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (kt0 + 2 * kKB < kend) fetch(sm0, kt0 + 2 * kKB);
+    tile(sm1, kt0 + kKB);
+  }
 
   // Partials: lane holds O^T[d = 16*dt + 4g + i][query lane%16].
 #pragma unroll
@@ -287,8 +260,8 @@ __global__ __launch_bounds__(128) void k_attn_f32(AttnArgs a) {
   const int qp = pos0 + q / G;
   const int kbeg = split * a.ks, kend = min(qp + 1, kbeg + a.ks);
   const int qrow = row0 + q / G, qcol = (kvh * G + q % G) * HD;
-  const float* kb = (const float*)a.kc + (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
-  const float* vb = (const float*)a.vc + (size_t)(b * a.n_kv + kvh) * a.max_len * HD;
+  const float* kb = (const float*)a.kc + (size_t)(b * a.n_kv + kvh) * a.kv_len * HD;
+  const float* vb = (const float*)a.vc + (size_t)(b * a.n_kv + kvh) * a.kv_len * HD;
   float qr[HD], o[HD];
 #pragma unroll
   for (int d = 0; d < HD; d += 4) {
@@ -395,7 +368,31 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a, int hd) {
     put_operand4<DT>(a.out, a.out2, row, head * hd + 64 + 4 * (lane - 16), qd, x);
 }
 
+// Row-major copy of cached positions: one thread per (plane, head, position,
+// dim) element.
+__global__ __launch_bounds__(256) void k_export_kv(const uint16_t* __restrict__ hi, const uint16_t* __restrict__ lo,
+                                                   int hd, int n_kv, int kv_len, int pos0, int npos, bool is_v,
+                                                   uint16_t* __restrict__ dst) {
+  const size_t per_plane = (size_t)n_kv * npos * hd;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= 2 * per_plane) return;
+  const int pl = (int)(i / per_plane);
+  const size_t r = i % per_plane;
+  const int head = (int)(r / ((size_t)npos * hd)), p = (int)(r / hd % npos), d = (int)(r % hd);
+  const size_t src = (size_t)head * kv_len * hd + (is_v ? v_elem(pos0 + p, d, hd) : k_elem(pos0 + p, d, hd));
+  dst[i] = (pl ? lo : hi)[src];
+}
+
 }  // namespace
+
+hipError_t launch_export_kv(const void* src_hi, const void* src_lo, int hd, int n_kv, int kv_len, int pos0,
+                            int npos, bool is_v, void* dst, hipStream_t st) {
+  const size_t n = (size_t)2 * n_kv * npos * hd;
+  if (n == 0) return hipSuccess;
+  k_export_kv<<<(unsigned)((n + 255) / 256), 256, 0, st>>>((const uint16_t*)src_hi, (const uint16_t*)src_lo, hd, n_kv,
+                                                           kv_len, pos0, npos, is_v, (uint16_t*)dst);
+  return hipGetLastError();
+}
 
 hipError_t launch_attention(int dtype, const AttnArgs& a, int n_qgroups, hipStream_t st) {
   const int groups = a.nseg * a.n_kv;

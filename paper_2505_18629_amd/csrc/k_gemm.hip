@@ -107,13 +107,13 @@ RV_DEV void epilogue(const GemmArgs& a, int tile0, int kg, int tok, int lane, f3
           put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + dim, a.n_heads * a.hd, rot);
         } else {
           const int b = a.row_seq[tok];
-          put_kv4<DT>(a.kc, a.kc2, ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim, rot);
+          put_k4<DT>(a.kc, a.kc2, (size_t)(b * a.n_kv + head) * a.kv_len * a.hd, pos, dim, a.hd, rot);
         }
       } else {
         const int rel = p0 - a.q_rows - a.k_rows + 4 * g;
         const int head = rel / a.hd, dim = rel % a.hd;
         const int b = a.row_seq[tok];
-        put_kv4<DT>(a.vc, a.vc2, ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim, v[nt]);
+        put_v4<DT>(a.vc, a.vc2, (size_t)(b * a.n_kv + head) * a.kv_len * a.hd, pos, dim, a.hd, v[nt]);
       }
     }
   }

@@ -82,11 +82,12 @@ struct rv_model {
 struct rv_cache {
   rv_model* m;
   int B, max_len, max_block, max_drafts;
+  int kv_len;  // cached positions per (sequence, kv head): max_len rounded up to whole 64-key tiles
   char* base;
   size_t bytes;
   int rows_cap, out_rows_cap, r1_cap, nchunk;
   size_t kv_layer_elems;
-  char* kc;   // K cache [layer][b][kv_head][pos][hd]: bf16 hi plane, or fp32
+  char* kc;   // K cache [layer][b][kv_head][kv_len x hd] (order: put_k4 / put_v4): bf16 hi plane, or fp32
   char* vc;
   char* kc2;  // bf16 lo planes (bf16 models)
   char* vc2;
@@ -184,7 +185,8 @@ size_t cache_layout(rv_cache* c, void* buf) {
   c->out_rows_cap = round_up(c->B * 2 * (c->max_drafts + 1), 64);
   c->r1_cap = c->B * (c->max_drafts + 1);
   c->nchunk = (mc.vocab + kVocabChunk - 1) / kVocabChunk;
-  c->kv_layer_elems = (size_t)c->B * mc.n_kv_heads * c->max_len * hd;
+  c->kv_len = round_up(c->max_len, 64);
+  c->kv_layer_elems = (size_t)c->B * mc.n_kv_heads * c->kv_len * hd;
   c->part_entries = (size_t)c->rows_cap * mc.n_heads * kSplitsPerQuery;
   const int nseg_cap = std::max(c->B, (int)RV_MAX_SEGS);
   Carve cv(buf);
@@ -406,7 +408,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, b
   at.n_heads = mc.n_heads;
   at.n_kv = mc.n_kv_heads;
   at.hd = hd;
-  at.max_len = c->max_len;
+  at.kv_len = c->kv_len;
   at.ks = ks;
   at.nsplit = nsplit;
   at.qmax = qmax;
@@ -450,7 +452,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, b
     g.hd = hd;
     g.n_heads = mc.n_heads;
     g.n_kv = mc.n_kv_heads;
-    g.max_len = c->max_len;
+    g.kv_len = c->kv_len;
     g.q_rows = m->qkv.q_rows;
     g.k_rows = m->qkv.k_rows;
     {
@@ -466,7 +468,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, b
         g.ldy = g.N;
         int gk = 1;
         HIP_TRY(run_gemm(c, EPI_RESID, g, true, st, &gk), "qkv");
-        QkvFinish qf{c->gpart, gk, M, g.N, g.q_rows, g.k_rows, hd, mc.n_heads, mc.n_kv_heads, c->max_len,
+        QkvFinish qf{c->gpart, gk, M, g.N, g.q_rows, g.k_rows, hd, mc.n_heads, mc.n_kv_heads, c->kv_len,
                      c->row_pos, c->row_seq, c->rope_cos, c->rope_sin, c->qbuf, c->qbuf2, kc, vc, kc2, vc2};
         HIP_TRY(launch_qkv_finish(dt, qf, st), "qkv finish");
       } else {
@@ -1004,18 +1006,22 @@ rv_status rv_debug_export_kv(const rv_cache* c, int32_t layer, int32_t seq, int3
   const int planes = es == 2 ? 2 : 1;
   const size_t plane = row * mc.n_kv_heads;
   if (dst_bytes < plane * planes) return fail(RV_E_BUFFER, "destination needs %zu bytes", plane * planes);
-  const size_t off = ((size_t)layer * c->kv_layer_elems + (size_t)seq * mc.n_kv_heads * c->max_len * hd +
-                      (size_t)pos0 * hd) * es;
-  const size_t spitch = (size_t)c->max_len * hd * es;
+  const size_t blk = (size_t)layer * c->kv_layer_elems + (size_t)seq * mc.n_kv_heads * c->kv_len * hd;
   hipStream_t st = (hipStream_t)stream;
-  for (int pl = 0; pl < planes; ++pl) {
-    const char* ks = (pl ? c->kc2 : c->kc) + off;
-    const char* vs = (pl ? c->vc2 : c->vc) + off;
-    HIP_TRY(hipMemcpy2DAsync((char*)d_k + pl * plane, row, ks, spitch, row, mc.n_kv_heads, hipMemcpyDeviceToDevice, st),
-            "copy");
-    HIP_TRY(hipMemcpy2DAsync((char*)d_v + pl * plane, row, vs, spitch, row, mc.n_kv_heads, hipMemcpyDeviceToDevice, st),
-            "copy");
+  if (es == 2) {
+    // bf16 caches are stored in attention operand order: copy out row-major
+    HIP_TRY(launch_export_kv((uint16_t*)c->kc + blk, (uint16_t*)c->kc2 + blk, (int)hd, mc.n_kv_heads, c->kv_len, pos0,
+                             npos, false, d_k, st),
+            "export");
+    HIP_TRY(launch_export_kv((uint16_t*)c->vc + blk, (uint16_t*)c->vc2 + blk, (int)hd, mc.n_kv_heads, c->kv_len, pos0,
+                             npos, true, d_v, st),
+            "export");
+    return RV_OK;
   }
+  const size_t off = (blk + (size_t)pos0 * hd) * es;
+  const size_t spitch = (size_t)c->kv_len * hd * es;
+  HIP_TRY(hipMemcpy2DAsync(d_k, row, c->kc + off, spitch, row, mc.n_kv_heads, hipMemcpyDeviceToDevice, st), "copy");
+  HIP_TRY(hipMemcpy2DAsync(d_v, row, c->vc + off, spitch, row, mc.n_kv_heads, hipMemcpyDeviceToDevice, st), "copy");
   return RV_OK;
 }
 

@@ -85,20 +85,61 @@ template <> RV_DEV void put_operand4<RV_F32>(void* hi, void*, int t, int k, int 
   memcpy((char*)hi + operand_offset(t, k, K, 4), &x, 16);
 }
 
-// K/V cache rows use the same operand form, in two row-major planes.
-template <int DT> RV_DEV void put_kv4(void* hi, void* lo, size_t i, const f32x4_t& x);
-template <> RV_DEV void put_kv4<RV_BF16>(void* hi, void* lo, size_t i, const f32x4_t& x) {
+// K/V cache.  Each (sequence, kv head) owns kv_len positions (a multiple of
+// 64) of hd values.  fp32 models store them row-major.  bf16 models store hi
+// and lo planes in the order the attention MFMAs consume them, so that a
+// 64-key tile is one contiguous span per plane and every operand is one
+// 16-byte LDS read per lane:
+//  K: 16-position blocks; unit (block, 32-dim chunk c) is 1 KiB, lane l
+//     holding positions 16*block + l%16, dims 32c + 8*(l/16) .. +7 (the A
+//     operand of S^T = K Q^T).
+//  V: 32-position blocks; unit (block, 16-dim tile t) is 1 KiB, lane l
+//     holding dim 16t + l%16 of the 8 keys of slot group g = l/16: keys
+//     4g..4g+3 and 16+4g..16+4g+3 of the block (the A operand of
+//     O^T += V^T P^T, whose B operand comes straight from the score
+//     registers in that key order).
+RV_DEV __host__ inline size_t k_elem(int pos, int d, int hd) {
+  return ((size_t)(pos >> 4) * (hd >> 5) + (d >> 5)) * 512 + ((pos & 15) + 16 * ((d & 31) >> 3)) * 8 + (d & 7);
+}
+RV_DEV __host__ inline size_t v_elem(int pos, int d, int hd) {
+  const int kk = pos & 31;
+  return ((size_t)(pos >> 5) * (hd >> 4) + (d >> 4)) * 512 + ((d & 15) + 16 * ((kk & 15) >> 2)) * 8 + (kk & 3) +
+         4 * (kk >> 4);
+}
+
+// Stores x = dims d..d+3 (d % 4 == 0) of position pos into the K or V cache
+// block starting at element `base`.
+template <int DT> RV_DEV void put_k4(void* hi, void* lo, size_t base, int pos, int d, int hd, const f32x4_t& x);
+template <int DT> RV_DEV void put_v4(void* hi, void* lo, size_t base, int pos, int d, int hd, const f32x4_t& x);
+template <>
+RV_DEV void put_k4<RV_BF16>(void* hi, void* lo, size_t base, int pos, int d, int hd, const f32x4_t& x) {
   uint16_t h[4], l[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     h[j] = f2bf(x[j]);
     l[j] = f2bf(x[j] - bf2f(h[j]));
   }
+  const size_t i = base + k_elem(pos, d, hd);  // the 4 dims are adjacent
   memcpy((uint16_t*)hi + i, h, 8);
   memcpy((uint16_t*)lo + i, l, 8);
 }
-template <> RV_DEV void put_kv4<RV_F32>(void* hi, void*, size_t i, const f32x4_t& x) {
-  memcpy((float*)hi + i, &x, 16);
+template <>
+RV_DEV void put_v4<RV_BF16>(void* hi, void* lo, size_t base, int pos, int d, int hd, const f32x4_t& x) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint16_t h = f2bf(x[j]);
+    const size_t i = base + v_elem(pos, d + j, hd);  // 8 elements apart
+    ((uint16_t*)hi)[i] = h;
+    ((uint16_t*)lo)[i] = f2bf(x[j] - bf2f(h));
+  }
+}
+template <>
+RV_DEV void put_k4<RV_F32>(void* hi, void*, size_t base, int pos, int d, int hd, const f32x4_t& x) {
+  memcpy((float*)hi + base + (size_t)pos * hd + d, &x, 16);
+}
+template <>
+RV_DEV void put_v4<RV_F32>(void* hi, void*, size_t base, int pos, int d, int hd, const f32x4_t& x) {
+  memcpy((float*)hi + base + (size_t)pos * hd + d, &x, 16);
 }
 
 // ---------------------------------------------------------------- packing

@@ -44,7 +44,7 @@ struct GemmArgs {
   // EPI_QKV
   void* qbuf;         // rotated q operand [rows][Hq*hd] (hi plane / fp32)
   void* qbuf2;        // lo plane
-  void* kc;           // this layer's K cache [B][Hkv][max_len][hd]: hi plane (or fp32)
+  void* kc;           // this layer's K cache [B][Hkv][kv_len x hd] (layout: put_k4): hi plane (or fp32)
   void* vc;
   void* kc2;          // lo planes (bf16 models)
   void* vc2;
@@ -52,7 +52,7 @@ struct GemmArgs {
   const int* row_seq;
   const float* rope_cos;  // [max_len][hd/2]
   const float* rope_sin;
-  int hd, n_heads, n_kv, max_len, q_rows, k_rows;
+  int hd, n_heads, n_kv, kv_len, q_rows, k_rows;
   MatDesc md;
 };
 // nt: row tiles per workgroup (1, 2, 4 or 8, and 3 or 6 for EPI_PARTIAL; even for SWIGLU);
@@ -70,7 +70,7 @@ hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int nt, int mt, hipStre
 struct AttnArgs {
   const void* q;        // rotated q operand [rows][Hq*hd] (hi plane / fp32)
   const void* q2;       // lo plane
-  const void* kc;       // layer base of the K cache: hi plane (or fp32)
+  const void* kc;       // layer base of the K cache: hi plane (or fp32); [B][Hkv][kv_len x hd], layout: put_k4
   const void* vc;
   const void* kc2;      // lo planes (bf16 models)
   const void* vc2;
@@ -79,7 +79,7 @@ struct AttnArgs {
   const int* seg_n;
   const int* seg_pos0;
   int nseg;
-  int n_heads, n_kv, hd, max_len;
+  int n_heads, n_kv, hd, kv_len;
   int ks;               // keys per split (multiple of 64)
   int nsplit;
   int qmax;             // query stride per (segment, kv head) in the partial buffers
@@ -91,6 +91,11 @@ struct AttnArgs {
 };
 hipError_t launch_attention(int dtype, const AttnArgs& a, int n_qgroups, hipStream_t st);
 hipError_t launch_attn_combine(int dtype, const AttnArgs& a, hipStream_t st);
+// Copies positions pos0 .. pos0+npos-1 of every kv head of one sequence out of
+// a bf16 K (is_v false) or V cache block into row-major planes
+// dst[2][n_kv][npos][hd] (hi, lo).  src: the sequence's first (kv head) block.
+hipError_t launch_export_kv(const void* src_hi, const void* src_lo, int hd, int n_kv, int kv_len, int pos0,
+                            int npos, bool is_v, void* dst, hipStream_t st);
 
 // ---------------------------------------------------------------- norms and planning
 // RMSNorm of rows of the fp32 residual h into matmul operands (out, out2).  Output row r
@@ -113,7 +118,7 @@ RV_DEV inline int kb_prefix(const uint8_t* kb, int b) {
 struct QkvFinish {
   const float* P;        // [gk][M][N] partials of the packed QKV matrix (physical rows)
   int gk, M, N;
-  int q_rows, k_rows, hd, n_heads, n_kv, max_len;
+  int q_rows, k_rows, hd, n_heads, n_kv, kv_len;
   const int* row_pos;
   const int* row_seq;
   const float* rope_cos;
@@ -170,16 +175,16 @@ RV_DEV void qkv_finish_unit(const QkvFinish& a, int tok, int tile, int r0) {
       put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + d1, a.n_heads * a.hd, o1);
       put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + d2, a.n_heads * a.hd, o2);
     } else {
-      const size_t kr = ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd;
-      put_kv4<DT>(a.kc, a.kc2, kr + d1, o1);
-      put_kv4<DT>(a.kc, a.kc2, kr + d2, o2);
+      const size_t kb = (size_t)(b * a.n_kv + head) * a.kv_len * a.hd;
+      put_k4<DT>(a.kc, a.kc2, kb, pos, d1, a.hd, o1);
+      put_k4<DT>(a.kc, a.kc2, kb, pos, d2, a.hd, o2);
     }
   } else {
     const int rel = p0 - a.q_rows - a.k_rows;
     const int head = rel / a.hd, dim = rel % a.hd;
-    const size_t vr = ((size_t)(b * a.n_kv + head) * a.max_len + pos) * a.hd + dim;
-    put_kv4<DT>(a.vc, a.vc2, vr + r0, x1);
-    put_kv4<DT>(a.vc, a.vc2, vr + 8 + r0, x2);
+    const size_t vb = (size_t)(b * a.n_kv + head) * a.kv_len * a.hd;
+    put_v4<DT>(a.vc, a.vc2, vb, pos, dim + r0, a.hd, x1);
+    put_v4<DT>(a.vc, a.vc2, vb, pos, dim + 8 + r0, a.hd, x2);
   }
 }
 
