@@ -38,7 +38,7 @@ constexpr int kKB = 64;  // keys per LDS tile
 // range hold finite values (the cache starts zeroed) and are masked (score
 // -inf, so P is exactly 0) or belong to queries whose results are not stored.
 template <int HD, int NW, int TPW>
-__global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
+__global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a, int n_qg) {
   static_assert(NW * TPW == 8, "a workgroup covers 128 queries");
   constexpr int DC = HD / 32;                 // d chunks for QK^T
   constexpr int DT = HD / 16;                 // d tiles for PV
@@ -49,7 +49,14 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t sm0[4][SPAN];
   __shared__ __attribute__((aligned(16))) uint16_t sm1[4][SPAN];
 
-  const int split = blockIdx.x, qg = blockIdx.y, grp = blockIdx.z;
+  // Workgroup -> (key split, query group, segment x kv head): the n_qg query
+  // groups of one (split, group) read the same K/V tiles, so they get
+  // indices 8 apart -- the same XCD (workgroup i runs on XCD i % 8) at about
+  // the same time -- and share its L2.
+  const int j = blockIdx.x / 8;
+  const int unit = (j / n_qg) * 8 + blockIdx.x % 8, qg = j % n_qg;
+  if (unit >= a.nsplit * a.nseg * a.n_kv) return;
+  const int split = unit % a.nsplit, grp = unit / a.nsplit;
   const int seg = grp / a.n_kv, kvh = grp % a.n_kv;
   const int G = a.n_heads / a.n_kv;
   const int nrows = a.seg_n[seg], row0 = a.seg_row0[seg], pos0 = a.seg_pos0[seg], b = a.seg_b[seg];
@@ -397,11 +404,12 @@ hipError_t launch_export_kv(const void* src_hi, const void* src_lo, int hd, int 
 hipError_t launch_attention(int dtype, const AttnArgs& a, int n_qgroups, hipStream_t st) {
   const int groups = a.nseg * a.n_kv;
   if (dtype == RV_BF16) {
-    dim3 grid(a.nsplit, n_qgroups, groups);
+    const unsigned units = (unsigned)(a.nsplit * groups);
+    const dim3 grid((units + 7) / 8 * 8 * n_qgroups);
     switch (a.hd) {
-      case 32: k_attn_bf16<32, 8, 1><<<grid, 512, 0, st>>>(a); break;
-      case 64: k_attn_bf16<64, 8, 1><<<grid, 512, 0, st>>>(a); break;
-      case 128: k_attn_bf16<128, 8, 1><<<grid, 512, 0, st>>>(a); break;
+      case 32: k_attn_bf16<32, 8, 1><<<grid, 512, 0, st>>>(a, n_qgroups); break;
+      case 64: k_attn_bf16<64, 8, 1><<<grid, 512, 0, st>>>(a, n_qgroups); break;
+      case 128: k_attn_bf16<128, 8, 1><<<grid, 512, 0, st>>>(a, n_qgroups); break;
       default: return hipErrorInvalidValue;
     }
   } else {
