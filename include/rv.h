@@ -123,8 +123,10 @@ rv_status rv_init_weights(const rv_config* cfg, uint64_t seed, void* d_buf, size
 void rv_model_free(rv_model* m);
 
 /* Bytes of device memory for a cache of `batch` sequences of up to max_len
- * positions: the KV cache [layer][b][kv_head][pos][head_dim] (fp32; for
- * bf16 models a bf16 hi plane plus a bf16 lo plane, value = hi + lo), the
+ * positions: the KV cache [layer][b][kv_head] x (max_len rounded up to a
+ * multiple of 64) positions x head_dim (fp32 row-major; for bf16 models a
+ * bf16 hi plane plus a bf16 lo plane, value = hi + lo, each in the order the
+ * attention kernel reads it -- rv_debug_export_kv returns rows), the
  * token-id history [b][max_len] (int32), the rotary table and the per-call
  * workspace for blocks of up to max_block rows per sequence and up to
  * max_drafts draft tokens. */
