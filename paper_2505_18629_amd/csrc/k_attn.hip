@@ -130,22 +130,29 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a, int n_qg) {
     for (int t = 0; t < TPW; ++t)
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) s[t][kt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // per 32-dim chunk: the 8 K operands first, then the three products as
+    // three passes over the 4 key blocks, so dependent MFMAs are 4 apart
 #pragma unroll
-    for (int c = 0; c < DC; ++c)
+    for (int c = 0; c < DC; ++c) {
+      bf16x8_t kh[4], kl[4];
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
         const int ko = (kt * DC + c) * 512 + lane * 8;
-        const bf16x8_t kh = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[0][ko]));
-        const bf16x8_t kl = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[1][ko]));
-#pragma unroll
-        for (int t = 0; t < TPW; ++t) {
-          const bf16x8_t qh = __builtin_bit_cast(bf16x8_t, qB[0][t][c]);
-          const bf16x8_t ql = __builtin_bit_cast(bf16x8_t, qB[1][t][c]);
-          s[t][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, qh, s[t][kt], 0, 0, 0);
-          s[t][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh, ql, s[t][kt], 0, 0, 0);
-          s[t][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kl, qh, s[t][kt], 0, 0, 0);
-        }
+        kh[kt] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[0][ko]));
+        kl[kt] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[1][ko]));
       }
+#pragma unroll
+      for (int t = 0; t < TPW; ++t) {
+        const bf16x8_t qh = __builtin_bit_cast(bf16x8_t, qB[0][t][c]);
+        const bf16x8_t ql = __builtin_bit_cast(bf16x8_t, qB[1][t][c]);
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) s[t][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh[kt], qh, s[t][kt], 0, 0, 0);
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) s[t][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kh[kt], ql, s[t][kt], 0, 0, 0);
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) s[t][kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kl[kt], qh, s[t][kt], 0, 0, 0);
+      }
+    }
 
       // online softmax in log2 units: p = 2^(s*scale - m), m the running
       // maximum of the scaled scores (scaling by a positive constant keeps the
@@ -209,15 +216,21 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a, int n_qg) {
           phi[j] = __builtin_bit_cast(__bf16, hb);
           plo[j] = __builtin_bit_cast(__bf16, lb);
         }
+        // the 2*DT V operands first, then the three products as three passes
+        // over the d tiles, so dependent MFMAs are DT apart
+        bf16x8_t vh[DT], vl[DT];
 #pragma unroll
         for (int d = 0; d < DT; ++d) {
           const int vo = (c * DT + d) * 512 + lane * 8;
-          const bf16x8_t vh = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[2][vo]));
-          const bf16x8_t vl = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[3][vo]));
-          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh, phi, O[t][d], 0, 0, 0);
-          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh, plo, O[t][d], 0, 0, 0);
-          O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vl, phi, O[t][d], 0, 0, 0);
+          vh[d] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[2][vo]));
+          vl[d] = __builtin_bit_cast(bf16x8_t, *(const uint4*)(&sm[3][vo]));
         }
+#pragma unroll
+        for (int d = 0; d < DT; ++d) O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh[d], phi, O[t][d], 0, 0, 0);
+#pragma unroll
+        for (int d = 0; d < DT; ++d) O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vh[d], plo, O[t][d], 0, 0, 0);
+#pragma unroll
+        for (int d = 0; d < DT; ++d) O[t][d] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vl[d], phi, O[t][d], 0, 0, 0);
       }
   };
 
