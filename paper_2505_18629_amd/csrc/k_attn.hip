@@ -2,7 +2,8 @@
 //
 // Every query row at position p of sequence b attends the cached keys
 // 0..p of b.  The K/V of the current block were written to the cache by the
-// QKV epilogue of the same layer, so this causal limit is the whole mask:
+// same layer's QKV matmul epilogue (or, after a K-split QKV matmul, by the
+// QKV finish kernel), so this causal limit is the whole mask:
 // the first draft copy cannot see the probe that follows it (the paper's
 // argument for unidirectional attention, Section 3.1), and the probe and
 // second copy see everything before them.
