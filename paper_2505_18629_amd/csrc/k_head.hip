@@ -214,16 +214,35 @@ __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
 // One 256-thread workgroup per sequence.  Wave w merges the chunk statistics
 // of fused rows w, w+4, ...: lane c takes chunks c and c+64, then the wave
 // merges lanes in a fixed butterfly order.  Thread 0 then applies the rule.
-__global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
+__global__ __launch_bounds__(512) void k_accept(HeadArgs a) {
   const int b = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int kb = a.kb[b], k1 = kb + 1, R1 = a.R1, Kb = kb_prefix(a.kb, b);
   const int zrow0 = b + Kb;  // first fused row of sequence b
+  const int* x = a.drafts + (size_t)b * a.k;
   __shared__ int xhat[RV_MAX_DRAFTS + 1];
+  __shared__ int xs[RV_MAX_DRAFTS];
   __shared__ float top2[RV_MAX_DRAFTS + 1];
   __shared__ float lse_z[RV_MAX_DRAFTS + 1];
   __shared__ float ent[2][RV_MAX_DRAFTS + 1];
-  for (int i = w; i < k1; i += 4) {
+  __shared__ float zx[RV_MAX_DRAFTS];        // fused logit of draft i at row i
+  __shared__ float qx[RV_MAX_DRAFTS];        // draft probability of draft i (sampling rule)
+  __shared__ float zh[RV_MAX_DRAFTS + 1];    // fused logit of row i's argmax
+  // One wave per row (k1 <= 8 with 8 waves): merge the chunk statistics.
+  // The same wave also fetches everything the accept decision reads of its
+  // row, so the serial tail below touches shared memory only.
+  for (int i = w; i < k1; i += 8) {
     const int row = zrow0 + i;
+    const float* zi = a.z + (size_t)row * a.V;
+    // draft id and its fused logit / probability, fetched beside the merge
+    int xi = 0;
+    float zxi = 0.f, qxi = 0.f;
+    if (lane == 0 && i < kb) {
+      xi = x[i];
+      if (xi >= 0 && xi < a.V) {  // out-of-range ids are reported through row_bad
+        zxi = zi[xi];
+        if (a.rule == RV_RULE_SAMPLING) qxi = a.q[((size_t)b * a.k + i) * a.V + xi];
+      }
+    }
     Stat st[3] = {{-INFINITY, 0.f, 0.f}, {-INFINITY, 0.f, 0.f}, {-INFINITY, 0.f, 0.f}};
     Top t{-INFINITY, 0x7fffffff, -INFINITY};
     for (int c = lane; c < a.nchunk; c += 64) {
@@ -252,14 +271,21 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
       t.i1 = min(max(t.i1, 0), a.V - 1);  // every id used as an index below is in range
       xhat[i] = t.i1;
       top2[i] = t.m2;
+      zh[i] = zi[t.i1];
       a.argmax[row] = t.i1;
+      if (i < kb) {
+        xs[i] = xi;
+        zx[i] = zxi;
+        qx[i] = qxi;
+      }
     }
   }
-  __syncthreads();
-  if (threadIdx.x != 0) return;
-  int bad = a.seq_bad[b];
+  // any out-of-range id in the sequence's block (or its history) voids it
   const int S = 1 + 2 * kb + a.n_probe + a.P, brow0 = b * (1 + a.n_probe + a.P) + 2 * Kb;
-  for (int j = 0; j < S; ++j) bad |= a.row_bad[brow0 + j];
+  int badv = threadIdx.x == 0 ? a.seq_bad[b] : 0;
+  for (int j = threadIdx.x; j < S; j += blockDim.x) badv |= a.row_bad[brow0 + j];
+  const int bad = __syncthreads_or(badv);
+  if (threadIdx.x != 0) return;
   float* mg = a.margins + (size_t)b * (a.k + 2);
   for (int i = 0; i < a.k + 2; ++i) mg[i] = NAN;
   if (bad) {
@@ -267,7 +293,6 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
     a.next_id[b] = -1;
     return;
   }
-  const int* x = a.drafts + (size_t)b * a.k;
   int n = kb;
   if (a.rule == RV_RULE_SAMPLING) {
     // reject at the first r_i * q_i(x_i) > p_i(x_i); t is drawn by k_sample
@@ -275,10 +300,9 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
       uint64_t c[4] = {(uint64_t)i, (uint64_t)b, 0ull, 0ull};
       philox4x64(c, a.seed, 0ull);
       const float r = uniform23(c[0]);
-      const float p = expf(a.z[((size_t)zrow0 + i) * a.V + x[i]] - lse_z[i]);
-      const float qx = a.q[((size_t)b * a.k + i) * a.V + x[i]];
-      mg[i] = qx > 0.f ? logf(p) - logf(r * qx) : INFINITY;
-      if (r * qx > p) {
+      const float p = expf(zx[i] - lse_z[i]);
+      mg[i] = qx[i] > 0.f ? logf(p) - logf(r * qx[i]) : INFINITY;
+      if (r * qx[i] > p) {
         n = i;
         break;
       }
@@ -291,7 +315,7 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
     const float log_eps = logf(a.eps), log_delta = logf(a.delta);
     const int src = a.ent_src == RV_ENTROPY_ORIGINAL ? 1 : 0;
     for (int i = 0; i < kb; ++i) {
-      const float lp = a.z[((size_t)zrow0 + i) * a.V + x[i]] - lse_z[i];
+      const float lp = zx[i] - lse_z[i];
       const float m = lp - fminf(log_eps, log_delta - ent[src][i]);
       mg[i] = m;
       if (!(m > 0.f)) {
@@ -301,27 +325,23 @@ __global__ __launch_bounds__(256) void k_accept(HeadArgs a) {
     }
   } else {
     for (int i = 0; i < kb; ++i) {
-      if (xhat[i] != x[i]) {
+      if (xhat[i] != xs[i]) {
         n = i;
         break;
       }
     }
     // margins of the tested drafts (inspection only)
-    for (int i = 0; i < min(n + 1, kb); ++i) {
-      const float* zi = a.z + ((size_t)zrow0 + i) * a.V;
-      const float zx = zi[x[i]];
-      mg[i] = xhat[i] == x[i] ? zx - top2[i] : zx - zi[xhat[i]];
-    }
+    for (int i = 0; i < min(n + 1, kb); ++i) mg[i] = xhat[i] == xs[i] ? zx[i] - top2[i] : zx[i] - zh[i];
   }
   const int t = xhat[n];
   a.accept_len[b] = n;
   a.next_id[b] = t;
   const int L = a.L[b];
   int* hist = a.ids + (size_t)b * a.max_len;
-  for (int i = 0; i < n; ++i) hist[L + i] = x[i];
+  for (int i = 0; i < n; ++i) hist[L + i] = xs[i];
   hist[L + n] = t;
   // bonus-token gap
-  mg[a.k + 1] = a.z[((size_t)zrow0 + n) * a.V + t] - top2[n];
+  mg[a.k + 1] = zh[n] - top2[n];
 }
 
 // Sampling rule: one workgroup per (vocabulary chunk, sequence).  Thread
@@ -440,7 +460,7 @@ __global__ __launch_bounds__(256) void k_logprob(HeadArgs a) {
 hipError_t launch_head(const HeadArgs& a, hipStream_t st) {
   const int R1 = a.R1;
   k_fuse_stats<<<dim3(a.nchunk, R1), 256, 0, st>>>(a);
-  k_accept<<<a.B, 256, 0, st>>>(a);
+  k_accept<<<a.B, 512, 0, st>>>(a);
   if (a.rule == RV_RULE_SAMPLING) {
     k_sample<<<dim3(a.nchunk, a.B), 256, 0, st>>>(a);
     k_sample_finish<<<a.B, 64, 0, st>>>(a);
