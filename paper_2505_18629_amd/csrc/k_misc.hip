@@ -85,10 +85,29 @@ __global__ void k_retile(const T* __restrict__ src, T* __restrict__ dst, int row
 }
 
 // ----------------------------------------------------------- embedding gather
+// d is a multiple of 128: each thread moves 8 (bf16) or 4 (fp32) elements
+// per 16-byte load.
 template <int DT>
 RV_DEV void gather_row(const typename Tr<DT>::T* embed, int tok, int d, float* dst) {
-  const typename Tr<DT>::T* e = embed + (size_t)tok * d;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) dst[i] = Tr<DT>::load(e[i]);
+  using T = typename Tr<DT>::T;
+  constexpr int V = 16 / sizeof(T);
+  const T* e = embed + (size_t)tok * d;
+  for (int i = threadIdx.x * V; i < d; i += blockDim.x * V) {
+    const u32x4 raw = *(const u32x4*)(e + i);
+    if constexpr (DT == RV_BF16) {
+      f32x4_t lo, hi;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        lo[j] = __uint_as_float(raw[j] << 16);
+        hi[j] = __uint_as_float(raw[j] & 0xffff0000u);
+      }
+      // element 2j is the low half of word j
+      *(f32x4_t*)(dst + i) = f32x4_t{lo[0], hi[0], lo[1], hi[1]};
+      *(f32x4_t*)(dst + i + 4) = f32x4_t{lo[2], hi[2], lo[3], hi[3]};
+    } else {
+      *(f32x4_t*)(dst + i) = __builtin_bit_cast(f32x4_t, raw);
+    }
+  }
 }
 
 // Verify block, one workgroup per (row j, sequence b):
