@@ -187,15 +187,15 @@ def cpu_baseline(w, lens, drafts, probe, layers=2):
     t0 = time.perf_counter()
     oracle.verify(sample, w.weight_seed, prefix, drafts[0], probe, w.alpha, w.prefix_pos)
     t_sample = time.perf_counter() - t0
-    # split the sample into per-layer and fixed (LM head, fusion) parts by a
-    # second run with one layer
+    # a second run with one layer: the oracle runs every layer but the last
+    # over all rows, the last (like the LM head) only on the block rows it
+    # returns, so L layers cost t_one + (L - 1) * (t_sample - t_one) / (layers - 1)
     one = shape.with_layers(1)
     t0 = time.perf_counter()
     oracle.verify(one, w.weight_seed, prefix, drafts[0], probe, w.alpha, w.prefix_pos)
     t_one = time.perf_counter() - t0
     per_layer = max(t_sample - t_one, 1e-9) / (layers - 1)
-    fixed = max(t_one - per_layer, 0.0)
-    t_step = fixed + per_layer * shape.n_layers
+    t_step = t_one + per_layer * (shape.n_layers - 1)
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     try:
         from threadpoolctl import threadpool_info

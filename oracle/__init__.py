@@ -225,13 +225,16 @@ def rope(x: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
 
-def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
-    """Softmax(q k^T / sqrt(hd)) v with row j attending keys 0..j; q head h
-    reads kv head h // (Hq / Hkv). q [n][Hq][hd], k/v [n][Hkv][hd]."""
-    n, Hq, hd = q.shape
+def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_pos=None) -> np.ndarray:
+    """Softmax(q k^T / sqrt(hd)) v where the query at position j attends keys
+    0..j; q head h reads kv head h // (Hq / Hkv).  q [m][Hq][hd] holds the
+    queries at positions q_pos (default 0..m-1), k/v [n][Hkv][hd] every key."""
+    m, Hq, hd = q.shape
+    n = k.shape[0]
     group = Hq // k.shape[1]
+    q_pos = np.arange(m) if q_pos is None else np.asarray(q_pos, dtype=np.int64)
     out = np.empty_like(q)
-    mask = np.triu(np.ones((n, n), dtype=bool), k=1)
+    mask = np.arange(n)[None, :] > q_pos[:, None]
     for h in range(Hq):
         kv = h // group
         s = (q[:, h, :] @ k[:, kv, :].T) / np.sqrt(hd)
@@ -272,27 +275,34 @@ def forward(shape, seed: int, tokens: Sequence[int], rows: Sequence[int], mode: 
     Hq, Hkv, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
     cos, sin = rope_table(shape, np.arange(n), rnd)
     h = embedding_rows(shape, seed, tokens)
+    rows = np.asarray(rows, dtype=np.int64)
     ks, vs = [], []
     for l in range(shape.n_layers):
+        # Only `rows` of the last layer's output are read, and under the causal
+        # mask a row's output depends on its own query and the keys and values
+        # at or before it; so that layer projects K and V for every token and
+        # runs the rest (query, attention, o-proj, MLP) on `rows` alone.
+        sel = rows if l == shape.n_layers - 1 else np.arange(n)
         a = rnd.operand(rms_norm(h, shape.rms_eps))
-        q = _matmul_wT(shape, seed, l, "q", a, rnd).reshape(n, Hq, hd)
+        q = _matmul_wT(shape, seed, l, "q", a[sel], rnd).reshape(len(sel), Hq, hd)
         k = _matmul_wT(shape, seed, l, "k", a, rnd).reshape(n, Hkv, hd)
         v = _matmul_wT(shape, seed, l, "v", a, rnd).reshape(n, Hkv, hd)
-        q = rnd.operand(rope(q, cos, sin))
+        q = rnd.operand(rope(q, cos[sel], sin[sel]))
         k = rnd.kv(rope(k, cos, sin))
         v = rnd.kv(v)
         if return_kv:
             ks.append(k)
             vs.append(v)
-        att = rnd.operand(causal_attention(q, k, v).reshape(n, Hq * hd))
-        h = rnd.f32(h + _matmul_wT(shape, seed, l, "o", att, rnd))
+        att = rnd.operand(causal_attention(q, k, v, sel).reshape(len(sel), Hq * hd))
+        h = rnd.f32(h[sel] + _matmul_wT(shape, seed, l, "o", att, rnd))
         a = rnd.operand(rms_norm(h, shape.rms_eps))
         g = _matmul_wT(shape, seed, l, "gate", a, rnd)
         u = _matmul_wT(shape, seed, l, "up", a, rnd)
         act = rnd.operand(silu(g) * u)
         h = rnd.f32(h + _matmul_wT(shape, seed, l, "down", act, rnd))
-    rows = np.asarray(rows, dtype=np.int64)
-    a = rnd.operand(rms_norm(h[rows], shape.rms_eps))
+    if shape.n_layers == 0:
+        h = h[rows]
+    a = rnd.operand(rms_norm(h, shape.rms_eps))
     logits = _matmul_wT(shape, seed, None, "lm_head", a, rnd)
     if return_kv:
         return logits, np.stack(ks), np.stack(vs)

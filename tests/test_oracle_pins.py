@@ -104,6 +104,23 @@ def test_forward_matches_library_llama(shape):
     assert np.abs(got - ref).max() < 1e-5 * np.abs(ref).max()
 
 
+@pytest.mark.parametrize("shape", PIN_SHAPES, ids=lambda s: s.name)
+def test_forward_at_scattered_rows_matches_library(monkeypatch, shape):
+    """The last layer runs only on the requested rows (the causal mask makes
+    each row's output independent of later rows): logits at a scattered,
+    unordered subset equal the library's logits at those positions."""
+    tokens = workload.random_ids(shape.vocab, 33, 7, 1)
+    ref = hf_logits(hf_llama(shape, 3), tokens)
+    rows = [32, 0, 17, 5, 31]
+    got = oracle.forward(shape, 3, tokens, rows, mode="exact")
+    assert np.abs(got - ref[rows]).max() < 1e-5 * np.abs(ref).max()
+    # a query masked as if it sat at the first rows' positions is caught
+    real = oracle.causal_attention
+    monkeypatch.setattr(oracle, "causal_attention", lambda q, k, v, q_pos=None: real(q, k, v, None))
+    bad = oracle.forward(shape, 3, tokens, rows, mode="exact")
+    assert np.abs(bad - ref[rows]).max() > 1e-3 * np.abs(ref).max()
+
+
 def _wrong_rope(x, cos, sin):
     half = x.shape[-1] // 2
     x1, x2 = x[..., :half], x[..., half:]
@@ -125,19 +142,19 @@ def test_planted_mistakes_break_the_pin(monkeypatch, mistake):
     elif mistake == "gqa_group":
         real = oracle.causal_attention
 
-        def interleaved(q, k, v):  # q head h -> kv head h % Hkv instead of h // G
+        def interleaved(q, k, v, q_pos=None):  # q head h -> kv head h % Hkv instead of h // G
             n, Hq, hd = q.shape
             Hkv = k.shape[1]
             kk = np.stack([k[:, h % Hkv] for h in range(Hq)], axis=1)
             vv = np.stack([v[:, h % Hkv] for h in range(Hq)], axis=1)
-            return real(q, kk, vv)
+            return real(q, kk, vv, q_pos)
         monkeypatch.setattr(oracle, "causal_attention", interleaved)
     elif mistake == "norm_eps_dropped":
         monkeypatch.setattr(oracle, "rms_norm", _wrong_norm)
     elif mistake == "silu_as_relu":
         monkeypatch.setattr(oracle, "silu", lambda x: np.maximum(x, 0.0))
     elif mistake == "causal_off":
-        def full(q, k, v):
+        def full(q, k, v, q_pos=None):
             n, Hq, hd = q.shape
             G = Hq // k.shape[1]
             out = np.empty_like(q)
