@@ -151,6 +151,23 @@ def test_tiny_bf16_gqa_matches_oracle(rv, gpu, alpha, P, n_probe, k):
 
 
 @pytest.mark.parametrize("shape", [workload.TINY, workload.TINY_GQA_BF16], ids=lambda s: s.name)
+@pytest.mark.parametrize("max_len", [128, 150])
+def test_block_fills_the_cache_exactly(rv, gpu, shape, max_len):
+    """Largest allowed prefix: sequence 0's block ends at the cache's last
+    position (max_len a multiple of the 64-key tile, and not), the block is
+    the cache's largest and the batch its full size."""
+    k, n_probe, P = 4, 6, 4
+    S = 1 + 2 * k + n_probe + P
+    lens = [max_len - S + 1, 57]
+    hists = [workload.random_ids(shape.vocab, L, 12, b) for b, L in enumerate(lens)]
+    drafts = [draft_case(shape, 3, h, k, 0.3, 120 + b) for b, h in enumerate(hists)]
+    probe = workload.random_ids(shape.vocab, n_probe, 12, 0xBEEF)
+    c = Case(rv, shape, 3, hists, drafts, probe, 0.3, P, max_len=max_len)
+    c.check(rv)
+    c.v.close()
+
+
+@pytest.mark.parametrize("shape", [workload.TINY, workload.TINY_GQA_BF16], ids=lambda s: s.name)
 @pytest.mark.parametrize("alpha,typical", [(0.3, (0.09, 0.3, "fused")), (1.0, (0.3, 0.1, "original")),
                                            (0.3, (float("inf"), 0.0, "fused")), (0.0, (0.05, 2.0, "fused"))])
 def test_typical_rule_matches_oracle(rv, gpu, shape, alpha, typical):
