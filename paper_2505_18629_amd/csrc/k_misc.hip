@@ -11,7 +11,9 @@ namespace {
 // the row and issues all its loads (h and the pending k-group partials of the
 // previous matmul, added in k-group order and written back to h) before
 // using any of them.
-template <int DT, int NPT>
+// PB: partials loaded per batch (2, 4 or 8: the smallest that covers pk, up
+// to 8), so that no more than pk - 1 loads per batch are repeats.
+template <int DT, int NPT, int PB>
 __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, const float* __restrict__ gain,
                                                   float eps, void* __restrict__ out, void* __restrict__ out2,
                                                   const int* __restrict__ gather, const float* __restrict__ P,
@@ -23,18 +25,18 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, 
 #pragma unroll
   for (int e = 0; e < NPT; ++e) v[e] = *(const f32x4_t*)(x + (threadIdx.x + e * blockDim.x) * 4);
   if (P) {
-    for (int g0 = 0; g0 < pk; g0 += 8) {
-      f32x4_t pv[NPT][8];
+    for (int g0 = 0; g0 < pk; g0 += PB) {
+      f32x4_t pv[NPT][PB];
 #pragma unroll
       for (int e = 0; e < NPT; ++e)
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
+        for (int u = 0; u < PB; ++u)
           pv[e][u] = *(const f32x4_t*)(P + ((size_t)min(g0 + u, pk - 1) * prows + src) * d +
                                        (threadIdx.x + e * blockDim.x) * 4);
 #pragma unroll
       for (int e = 0; e < NPT; ++e)
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[e] += g0 + u < pk ? pv[e][u] : f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int u = 0; u < PB; ++u) v[e] += g0 + u < pk ? pv[e][u] : f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
     for (int e = 0; e < NPT; ++e) *(f32x4_t*)(x + (threadIdx.x + e * blockDim.x) * 4) = v[e];
@@ -199,13 +201,19 @@ hipError_t launch_rmsnorm(int dtype, float* h, int rows, int d, const float* gai
   const int npt = d <= 4096 ? 1 : 2;
   const int threads = d / (4 * npt);
   if (threads > 1024 || threads % 64) return hipErrorInvalidValue;
-#define RV_NORM(DT_, N_) \
-  k_rmsnorm<DT_, N_><<<rows, threads, 0, st>>>(h, d, gain, eps, out, out2, gather, P, pk, prows)
+  const int pb = pk <= 2 ? 2 : pk <= 4 ? 4 : 8;
+#define RV_NORM(DT_, N_, PB_) \
+  k_rmsnorm<DT_, N_, PB_><<<rows, threads, 0, st>>>(h, d, gain, eps, out, out2, gather, P, pk, prows)
+#define RV_NORM_PB(DT_, N_)       \
+  if (pb == 2) RV_NORM(DT_, N_, 2); \
+  else if (pb == 4) RV_NORM(DT_, N_, 4); \
+  else RV_NORM(DT_, N_, 8)
   if (dtype == RV_BF16) {
-    if (npt == 1) RV_NORM(RV_BF16, 1); else RV_NORM(RV_BF16, 2);
+    if (npt == 1) { RV_NORM_PB(RV_BF16, 1); } else { RV_NORM_PB(RV_BF16, 2); }
   } else {
-    if (npt == 1) RV_NORM(RV_F32, 1); else RV_NORM(RV_F32, 2);
+    if (npt == 1) { RV_NORM_PB(RV_F32, 1); } else { RV_NORM_PB(RV_F32, 2); }
   }
+#undef RV_NORM_PB
 #undef RV_NORM
   return hipGetLastError();
 }
