@@ -11,8 +11,9 @@ namespace {
 // the row and issues all its loads (h and the pending k-group partials of the
 // previous matmul, added in k-group order and written back to h) before
 // using any of them.
-// PB: partials loaded per batch (2, 4 or 8: the smallest that covers pk, up
-// to 8), so that no more than pk - 1 loads per batch are repeats.
+// PB: partials loaded per batch, the smallest of 2, 4 and 8 that holds pk
+// (larger pk take several batches of 8); loads past pk repeat the last
+// partial and are not added.
 template <int DT, int NPT, int PB>
 __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, const float* __restrict__ gain,
                                                   float eps, void* __restrict__ out, void* __restrict__ out2,
