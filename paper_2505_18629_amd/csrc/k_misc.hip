@@ -66,14 +66,15 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, 
 
 // Completes a K-split QKV projection: sums the k-group partials (physical
 // row order of the packed QKV matrix) in order, applies rotate-half rotary to
-// q and k, and writes the q operand and the K/V cache rows.  One workgroup
-// per token; a thread handles rows r0..r0+3 of a 16-row tile and their
-// rotary partners r0+8..r0+11 (r0 in {0, 4}).
+// q and k, and writes the q operand and the K/V cache rows.  Workgroups of
+// 256 threads, gridDim.y of them per token; a thread handles rows r0..r0+3
+// of a 16-row tile and their rotary partners r0+8..r0+11 (r0 in {0, 4}).
 template <int DT>
-__global__ __launch_bounds__(1024) void k_qkv_finish(QkvFinish a) {
+__global__ __launch_bounds__(256) void k_qkv_finish(QkvFinish a) {
   const int tok = blockIdx.x;
   const int units = a.N / 8;
-  for (int u = threadIdx.x; u < units; u += blockDim.x) qkv_finish_unit<DT>(a, tok, u >> 1, (u & 1) * 4);
+  for (int u = blockIdx.y * blockDim.x + threadIdx.x; u < units; u += gridDim.y * blockDim.x)
+    qkv_finish_unit<DT>(a, tok, u >> 1, (u & 1) * 4);
 }
 
 // Row-major [rows][K] <-> operand tiles, one element per thread.
@@ -220,12 +221,14 @@ hipError_t launch_rmsnorm(int dtype, float* h, int rows, int d, const float* gai
 }
 
 hipError_t launch_qkv_finish(int dtype, const QkvFinish& a, hipStream_t st) {
+  // workgroups of 256 threads, one unit each, spread over as many
+  // workgroups per token as the units need (8B: 768 units, 3 per token)
   const int units = a.N / 8;
-  const int threads = std::min(1024, (units + 63) / 64 * 64);
+  const dim3 grid(a.M, (units + 255) / 256);
   if (dtype == RV_BF16)
-    k_qkv_finish<RV_BF16><<<a.M, threads, 0, st>>>(a);
+    k_qkv_finish<RV_BF16><<<grid, 256, 0, st>>>(a);
   else
-    k_qkv_finish<RV_F32><<<a.M, threads, 0, st>>>(a);
+    k_qkv_finish<RV_F32><<<grid, 256, 0, st>>>(a);
   return hipGetLastError();
 }
 
