@@ -8,9 +8,10 @@ namespace {
 // ----------------------------------------------------------- RMSNorm
 // y = h * rsqrt(mean(h^2) + eps) * g, stored as a matmul operand.  One
 // workgroup of d / (4 NPT) threads per row: every thread owns NPT float4s of
-// the row and issues all its loads (h and the pending k-group partials of the
-// previous matmul, added in k-group order and written back to h) before
-// using any of them.
+// the row and issues all its loads (the gains, h and the pending k-group
+// partials of the previous matmul, added in k-group order) before using any
+// of them.  The updated h is written back after the workgroup's reduction
+// barrier, so the barrier does not wait for that store.
 // PB: partials loaded per batch, the smallest of 2, 4 and 8 that holds pk
 // (larger pk take several batches of 8); loads past pk repeat the last
 // partial and are not added.
@@ -22,9 +23,12 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, 
   const int r = blockIdx.x;
   const int src = gather ? gather[r] : r;
   float* x = h + (size_t)src * d;
-  f32x4_t v[NPT];
+  f32x4_t v[NPT], gg[NPT];
 #pragma unroll
-  for (int e = 0; e < NPT; ++e) v[e] = *(const f32x4_t*)(x + (threadIdx.x + e * blockDim.x) * 4);
+  for (int e = 0; e < NPT; ++e) {
+    gg[e] = *(const f32x4_t*)(gain + (threadIdx.x + e * blockDim.x) * 4);
+    v[e] = *(const f32x4_t*)(x + (threadIdx.x + e * blockDim.x) * 4);
+  }
   if (P) {
     for (int g0 = 0; g0 < pk; g0 += PB) {
       f32x4_t pv[NPT][PB];
@@ -39,8 +43,6 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, 
 #pragma unroll
         for (int u = 0; u < PB; ++u) v[e] += g0 + u < pk ? pv[e][u] : f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
-#pragma unroll
-    for (int e = 0; e < NPT; ++e) *(f32x4_t*)(x + (threadIdx.x + e * blockDim.x) * 4) = v[e];
   }
   float ss = 0.f;
 #pragma unroll
@@ -53,13 +55,16 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, 
   float tot = 0.f;
   for (int w = 0; w < nw; ++w) tot += part[w];
   const float rs = 1.0f / sqrtf(tot / (float)d + eps);
+  if (P) {
+#pragma unroll
+    for (int e = 0; e < NPT; ++e) *(f32x4_t*)(x + (threadIdx.x + e * blockDim.x) * 4) = v[e];
+  }
 #pragma unroll
   for (int e = 0; e < NPT; ++e) {
     const int i = (threadIdx.x + e * blockDim.x) * 4;
-    const f32x4_t gg = *(const f32x4_t*)(gain + i);
     f32x4_t o;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) o[j] = v[e][j] * rs * gg[j];
+    for (int j = 0; j < 4; ++j) o[j] = v[e][j] * rs * gg[e][j];
     put_operand4<DT>(out, out2, r, i, d, o);
   }
 }
