@@ -69,17 +69,90 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, 
   }
 }
 
+// One finish unit: token tok, 16-row tile `tile` of the packed QKV matrix,
+// rows r0..r0+3 (r0 in {0, 4}) and their rotate-half partners r0+8..r0+11.
+// Sums the k-group partials in order, applies rotary to q and k rows, and
+// writes the q operand or the K/V cache rows.  The first PB k-groups' loads
+// are issued before the token's position is read (they do not depend on
+// it), so the rotary table loads are the only dependent round trip.
+template <int DT, int PB>
+RV_DEV void qkv_finish_unit(const QkvFinish& a, int tok, int tile, int r0) {
+  const int p0 = tile * 16;
+  auto part = [&](int g) { return a.P + ((size_t)g * a.M + tok) * a.N + p0; };
+  f32x4_t l1[PB], l2[PB];
+#pragma unroll
+  for (int v = 0; v < PB; ++v) {
+    const float* row = part(min(v, a.gk - 1));
+    l1[v] = *(const f32x4_t*)(row + r0);
+    l2[v] = *(const f32x4_t*)(row + 8 + r0);
+  }
+  const int pos = a.row_pos[tok], b = a.row_seq[tok];
+  f32x4_t x1 = {0.f, 0.f, 0.f, 0.f}, x2 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int v = 0; v < PB; ++v) {
+    if (v < a.gk) {
+      x1 += l1[v];
+      x2 += l2[v];
+    }
+  }
+  for (int g0 = PB; g0 < a.gk; g0 += 8) {  // more than PB (= 8) k-groups
+    f32x4_t m1[8], m2[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      const float* row = part(min(g0 + v, a.gk - 1));
+      m1[v] = *(const f32x4_t*)(row + r0);
+      m2[v] = *(const f32x4_t*)(row + 8 + r0);
+    }
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      if (g0 + v < a.gk) {
+        x1 += m1[v];
+        x2 += m2[v];
+      }
+    }
+  }
+  const int half = a.hd / 2;
+  if (p0 < a.q_rows + a.k_rows) {
+    const bool is_q = p0 < a.q_rows;
+    const int rel = is_q ? p0 : p0 - a.q_rows;
+    const int head = rel / a.hd, j = (rel % a.hd) >> 4;
+    const f32x4_t cs = *(const f32x4_t*)(a.rope_cos + (size_t)pos * half + 8 * j + r0);
+    const f32x4_t sn = *(const f32x4_t*)(a.rope_sin + (size_t)pos * half + 8 * j + r0);
+    f32x4_t o1, o2;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o1[i] = x1[i] * cs[i] - x2[i] * sn[i];
+      o2[i] = x2[i] * cs[i] + x1[i] * sn[i];
+    }
+    const int d1 = 8 * j + r0, d2 = half + 8 * j + r0;
+    if (is_q) {
+      put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + d1, a.n_heads * a.hd, o1);
+      put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + d2, a.n_heads * a.hd, o2);
+    } else {
+      const size_t kb = (size_t)(b * a.n_kv + head) * a.kv_len * a.hd;
+      put_k4<DT>(a.kc, a.kc2, kb, pos, d1, a.hd, o1);
+      put_k4<DT>(a.kc, a.kc2, kb, pos, d2, a.hd, o2);
+    }
+  } else {
+    const int rel = p0 - a.q_rows - a.k_rows;
+    const int head = rel / a.hd, dim = rel % a.hd;
+    const size_t vb = (size_t)(b * a.n_kv + head) * a.kv_len * a.hd;
+    put_v4<DT>(a.vc, a.vc2, vb, pos, dim + r0, a.hd, x1);
+    put_v4<DT>(a.vc, a.vc2, vb, pos, dim + 8 + r0, a.hd, x2);
+  }
+}
+
 // Completes a K-split QKV projection: sums the k-group partials (physical
 // row order of the packed QKV matrix) in order, applies rotate-half rotary to
 // q and k, and writes the q operand and the K/V cache rows.  Workgroups of
 // 256 threads, gridDim.y of them per token; a thread handles rows r0..r0+3
 // of a 16-row tile and their rotary partners r0+8..r0+11 (r0 in {0, 4}).
-template <int DT>
+template <int DT, int PB>
 __global__ __launch_bounds__(256) void k_qkv_finish(QkvFinish a) {
   const int tok = blockIdx.x;
   const int units = a.N / 8;
   for (int u = blockIdx.y * blockDim.x + threadIdx.x; u < units; u += gridDim.y * blockDim.x)
-    qkv_finish_unit<DT>(a, tok, u >> 1, (u & 1) * 4);
+    qkv_finish_unit<DT, PB>(a, tok, u >> 1, (u & 1) * 4);
 }
 
 // Row-major [rows][K] <-> operand tiles, one element per thread.
@@ -230,10 +303,14 @@ hipError_t launch_qkv_finish(int dtype, const QkvFinish& a, hipStream_t st) {
   // workgroups per token as the units need (8B: 768 units, 3 per token)
   const int units = a.N / 8;
   const dim3 grid(a.M, (units + 255) / 256);
-  if (dtype == RV_BF16)
-    k_qkv_finish<RV_BF16><<<grid, 256, 0, st>>>(a);
-  else
-    k_qkv_finish<RV_F32><<<grid, 256, 0, st>>>(a);
+  const int pb = a.gk <= 2 ? 2 : a.gk <= 4 ? 4 : 8;
+#define RV_FIN(DT_, PB_) k_qkv_finish<DT_, PB_><<<grid, 256, 0, st>>>(a)
+  if (dtype == RV_BF16) {
+    if (pb == 2) RV_FIN(RV_BF16, 2); else if (pb == 4) RV_FIN(RV_BF16, 4); else RV_FIN(RV_BF16, 8);
+  } else {
+    if (pb == 2) RV_FIN(RV_F32, 2); else if (pb == 4) RV_FIN(RV_F32, 4); else RV_FIN(RV_F32, 8);
+  }
+#undef RV_FIN
   return hipGetLastError();
 }
 

@@ -132,61 +132,6 @@ struct QkvFinish {
 };
 hipError_t launch_qkv_finish(int dtype, const QkvFinish& a, hipStream_t st);
 
-// One finish unit: token tok, 16-row tile `tile` of the packed QKV matrix,
-// rows r0..r0+3 (r0 in {0, 4}) and their rotate-half partners r0+8..r0+11.
-// Sums the k-group partials in order, applies rotary to q and k rows, and
-// writes the q operand or the K/V cache rows.
-template <int DT>
-RV_DEV void qkv_finish_unit(const QkvFinish& a, int tok, int tile, int r0) {
-  const int pos = a.row_pos[tok], b = a.row_seq[tok];
-  const int half = a.hd / 2;
-  const int p0 = tile * 16;
-  f32x4_t x1 = {0.f, 0.f, 0.f, 0.f}, x2 = {0.f, 0.f, 0.f, 0.f};
-  for (int g0 = 0; g0 < a.gk; g0 += 8) {
-    f32x4_t l1[8], l2[8];
-#pragma unroll
-    for (int v = 0; v < 8; ++v) {
-      const float* row = a.P + ((size_t)min(g0 + v, a.gk - 1) * a.M + tok) * a.N + p0;
-      l1[v] = *(const f32x4_t*)(row + r0);
-      l2[v] = *(const f32x4_t*)(row + 8 + r0);
-    }
-#pragma unroll
-    for (int v = 0; v < 8; ++v) {
-      if (g0 + v < a.gk) {
-        x1 += l1[v];
-        x2 += l2[v];
-      }
-    }
-  }
-  if (p0 < a.q_rows + a.k_rows) {
-    const bool is_q = p0 < a.q_rows;
-    const int rel = is_q ? p0 : p0 - a.q_rows;
-    const int head = rel / a.hd, j = (rel % a.hd) >> 4;
-    const float* cs = a.rope_cos + (size_t)pos * half + 8 * j + r0;
-    const float* sn = a.rope_sin + (size_t)pos * half + 8 * j + r0;
-    f32x4_t o1, o2;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      o1[i] = x1[i] * cs[i] - x2[i] * sn[i];
-      o2[i] = x2[i] * cs[i] + x1[i] * sn[i];
-    }
-    const int d1 = 8 * j + r0, d2 = half + 8 * j + r0;
-    if (is_q) {
-      put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + d1, a.n_heads * a.hd, o1);
-      put_operand4<DT>(a.qbuf, a.qbuf2, tok, head * a.hd + d2, a.n_heads * a.hd, o2);
-    } else {
-      const size_t kb = (size_t)(b * a.n_kv + head) * a.kv_len * a.hd;
-      put_k4<DT>(a.kc, a.kc2, kb, pos, d1, a.hd, o1);
-      put_k4<DT>(a.kc, a.kc2, kb, pos, d2, a.hd, o2);
-    }
-  } else {
-    const int rel = p0 - a.q_rows - a.k_rows;
-    const int head = rel / a.hd, dim = rel % a.hd;
-    const size_t vb = (size_t)(b * a.n_kv + head) * a.kv_len * a.hd;
-    put_v4<DT>(a.vc, a.vc2, vb, pos, dim + r0, a.hd, x1);
-    put_v4<DT>(a.vc, a.vc2, vb, pos, dim + 8 + r0, a.hd, x2);
-  }
-}
 
 // Converts operand planes between row-major [rows][K] and operand tiles.
 hipError_t launch_retile(int dtype, const void* src, void* dst, int rows, int K, bool to_tiles, hipStream_t st);
