@@ -317,13 +317,18 @@ __global__ __launch_bounds__(128) void k_attn_f32(AttnArgs a) {
 // One wave per query: lane s holds split s's running max and sum (at most 64
 // splits), so the merge weights come from two wave reductions; then each lane
 // accumulates two output dims over the splits in index order.  The first F
-// splits' values are loaded together with the statistics (F = 4, 8 or 16,
-// the smallest that covers the query's splits, chosen per wave); loads past
-// the last split read a valid duplicate and get weight 0, so every load is
-// unconditional; further splits follow in batches of 8.
+// splits' values are loaded before the reductions, together with the
+// statistics (F = 4, 8 or 16, the smallest that covers the query's splits,
+// chosen per wave); loads past the last split read a valid duplicate and get
+// weight 0, so every load is unconditional; further splits follow in batches
+// of 8.
 template <int F>
-RV_DEV void combine_accumulate(const AttnArgs& a, size_t e0, size_t stride, int ns, int hd, int d0, int d1, float f,
-                               float& acc0, float& acc1) {
+RV_DEV void combine_query(const AttnArgs& a, size_t e0, size_t stride, int ns, int hd, int lane, float& acc0,
+                          float& acc1, float& L) {
+  const int sl = min(lane, ns - 1);
+  const int d0 = min(lane, hd - 1), d1 = min(lane + 64, hd - 1);
+  const float ms = a.part_ml[2 * (e0 + sl * stride)];
+  const float ls = a.part_ml[2 * (e0 + sl * stride) + 1];
   float w0[F], w1[F];
 #pragma unroll
   for (int u = 0; u < F; ++u) {
@@ -331,6 +336,9 @@ RV_DEV void combine_accumulate(const AttnArgs& a, size_t e0, size_t stride, int 
     w0[u] = a.part_o[e * hd + d0];
     w1[u] = a.part_o[e * hd + d1];
   }
+  const float M = wave_max(lane < ns ? ms : -INFINITY);
+  const float f = (lane < ns && ms != -INFINITY) ? exp2f(ms - M) : 0.f;
+  L = wave_sum(ls * f);
 #pragma unroll
   for (int u = 0; u < F; ++u) {
     const float fu = u < ns ? __shfl(f, u, 64) : 0.f;
@@ -368,17 +376,10 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a, int hd) {
   const size_t stride = (size_t)(a.nseg * a.n_kv) * a.qmax;
   const size_t e0 = (size_t)grp * a.qmax + q;
   const int ns = min(a.nsplit, pos_q / a.ks + 1);  // splits that saw keys of this query
-  const int sl = min(lane, ns - 1);
-  const int d0 = min(lane, hd - 1), d1 = min(lane + 64, hd - 1);
-  const float ms = a.part_ml[2 * (e0 + sl * stride)];
-  const float ls = a.part_ml[2 * (e0 + sl * stride) + 1];
-  const float M = wave_max(lane < ns ? ms : -INFINITY);
-  const float f = (lane < ns && ms != -INFINITY) ? exp2f(ms - M) : 0.f;
-  const float L = wave_sum(ls * f);
-  float acc0 = 0.f, acc1 = 0.f;
-  if (ns <= 4) combine_accumulate<4>(a, e0, stride, ns, hd, d0, d1, f, acc0, acc1);
-  else if (ns <= 8) combine_accumulate<8>(a, e0, stride, ns, hd, d0, d1, f, acc0, acc1);
-  else combine_accumulate<16>(a, e0, stride, ns, hd, d0, d1, f, acc0, acc1);
+  float acc0 = 0.f, acc1 = 0.f, L;
+  if (ns <= 4) combine_query<4>(a, e0, stride, ns, hd, lane, acc0, acc1, L);
+  else if (ns <= 8) combine_query<8>(a, e0, stride, ns, hd, lane, acc0, acc1, L);
+  else combine_query<16>(a, e0, stride, ns, hd, lane, acc0, acc1, L);
   const float inv = 1.0f / L;
   const int row = a.seg_row0[seg] + q / G, head = kvh * G + q % G;
   const int qd = a.n_heads * hd;
