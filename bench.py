@@ -174,7 +174,7 @@ def build_state(rv, w, case=0):
     return v, [int(x) for x in lens], drafts, probe
 
 
-def cpu_baseline(w, lens, drafts, probe, layers=6):
+def cpu_baseline(w, lens, drafts, probe, layers=12):
     """The CPU oracle on a bounded sample of the same step: the from-scratch
     forward over prefix + block for `layers` of the model's layers plus the LM
     head on the 2(k+1) rows, fusion and accept, for sequence 0; the layer time
