@@ -32,20 +32,20 @@ CHECKED = {
 OUTS = ("o", "r", "z")
 
 
-@pytest.mark.parametrize("name", list(CHECKED))
-def test_workload_one_layer_matches_oracle(rv, gpu, name):
+@pytest.mark.parametrize("name,case", [(n, 0) for n in CHECKED] + [("8b-bf16-b1", 1), ("8b-bf16-b16-ragged", 1)])
+def test_workload_one_layer_matches_oracle(rv, gpu, name, case):
     import torch
     w = workload.WORKLOADS[name]
     shape = w.shape.with_layers(1)
-    lens = [int(x) for x in workload.prefix_lengths(w)]
-    prefixes = [[int(t) for t in p] for p in workload.prefix_ids(w, lens)]
+    lens = [int(x) for x in workload.prefix_lengths(w, case)]
+    prefixes = [[int(t) for t in p] for p in workload.prefix_ids(w, lens, case)]
     check = CHECKED[name](lens)
     S = w.rows_per_seq
-    print(f"\n{name}: batch {w.batch}, prefixes {min(lens)}..{max(lens)}, {S} rows per sequence, "
+    print(f"\n{name} case {case}: batch {w.batch}, prefixes {min(lens)}..{max(lens)}, {S} rows per sequence, "
           f"oracle on sequences {check}", flush=True)
     # random drafts; each checked sequence's first draft is the oracle's
     # greedy token after its prefix, so that alpha = 0 accepts it
-    drafts = np.stack([workload.random_ids(shape.vocab, w.k, w.index, 7, b) for b in range(w.batch)])
+    drafts = np.stack([workload.random_ids(shape.vocab, w.k, w.index, 7, case, b) for b in range(w.batch)])
     for b in check:
         drafts[b, 0] = int(np.argmax(oracle.forward(shape, w.weight_seed, prefixes[b], [lens[b] - 1])[0]))
     probe = workload.probe_ids(w)
