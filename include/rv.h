@@ -212,6 +212,27 @@ rv_status rv_verify_sampled(rv_cache* c, const int32_t* h_prefix_len, const int3
 
 /* ---- inspection (tests and benchmarks) ---- */
 
+/* The fusion, log-softmax and accept stage of rv_verify (Eq. 2; Algorithm 2,
+ * or Algorithm 3 with RV_RULE_TYPICAL; Appendix A) run by the same kernels
+ * on logits the caller supplies instead of the LM head's.
+ *   d_logits [batch][2(k+1)][vocab] device fp32: per sequence the original
+ *                rows o_1..o_{k+1}, then the reflective rows r_1..r_{k+1};
+ *                copied into the cache's logit rows.  Entries may be -inf
+ *                (an id ruled out) as long as every row has a finite entry;
+ *                where alpha is 0 or 1 the row weighted by 0 must be finite
+ *                (0 * inf is NaN in Eq. 2 as written).
+ *   h_prefix_len [batch] host: L_b; the decision is appended to the id
+ *                history at L_b .. L_b+n as rv_verify does (1 <= L_b and
+ *                L_b + k + 1 <= max_len).
+ *   d_draft_ids [batch][k] device int32 (NULL if k == 0), k <= max_drafts; a
+ *                sequence with an id outside [0, vocab) gets -1, -1.
+ *   fusion       as rv_verify (prefix_pos is not used; the sampling rule is
+ *                not available here).
+ * rv_debug_output then returns the rows of this call.  Asynchronous. */
+rv_status rv_debug_fuse_accept(rv_cache* c, const float* d_logits, const int32_t* h_prefix_len,
+                               const int32_t* d_draft_ids, int32_t k, const rv_fusion* fusion, int32_t* d_accept_len,
+                               int32_t* d_next_id, void* stream);
+
 /* Which result of the last verify to copy.  Per-row results have one row per
  * (sequence b, i = 1..k_b+1), sequence after sequence ([batch][k+1] when every
  * sequence has k drafts).  RV_OUT_ORIG .. RV_OUT_LOGP_FUSED are fp32 rows of
@@ -255,7 +276,10 @@ rv_status rv_debug_weight_bits(const rv_model* m, int32_t tensor, const int64_t*
 /* Intermediate activations of the last prefill or verify pass, for the
  * rows of that pass (row r = b*S + j for a verify block).  The values are
  * those of the final layer:
- *   RV_WS_RESID   fp32 [rows][d_model]     residual stream after the last layer
+ *   RV_WS_RESID   fp32 [rows][d_model]     residual stream: after a prefill, after the
+ *                 last layer; after a verify, before the last layer's down
+ *                 projection (the final norm adds that projection's k-group
+ *                 partials as it reads the rows the LM head needs)
  *   RV_WS_ATTN    operand [rows][n_heads*head_dim]  attention output (pre o-proj)
  *   RV_WS_ACT     operand [rows][ffn_dim]  SwiGLU output (pre down-proj)
  *   RV_WS_QUERY   operand [rows][n_heads*head_dim]  rotated queries

@@ -225,24 +225,31 @@ def rope(x: np.ndarray, cos: np.ndarray, sin: np.ndarray) -> np.ndarray:
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
 
-def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_pos=None) -> np.ndarray:
+def causal_attention(q: np.ndarray, k: np.ndarray, v: np.ndarray, q_pos=None, rows_per_chunk: int = 1024) -> np.ndarray:
     """Softmax(q k^T / sqrt(hd)) v where the query at position j attends keys
     0..j; q head h reads kv head h // (Hq / Hkv).  q [m][Hq][hd] holds the
-    queries at positions q_pos (default 0..m-1), k/v [n][Hkv][hd] every key."""
+    queries at positions q_pos (default 0..m-1), k/v [n][Hkv][hd] the keys at
+    positions 0..n-1.  Queries are taken rows_per_chunk at a time (each
+    query's softmax is independent of the others), and a chunk only forms
+    scores against the keys its latest query may see; the mask then removes
+    the later keys of the chunk's earlier queries."""
     m, Hq, hd = q.shape
-    n = k.shape[0]
     group = Hq // k.shape[1]
     q_pos = np.arange(m) if q_pos is None else np.asarray(q_pos, dtype=np.int64)
     out = np.empty_like(q)
-    mask = np.arange(n)[None, :] > q_pos[:, None]
-    for h in range(Hq):
-        kv = h // group
-        s = (q[:, h, :] @ k[:, kv, :].T) / np.sqrt(hd)
-        s[mask] = -np.inf
-        s = s - s.max(axis=1, keepdims=True)
-        p = np.exp(s)
-        p /= p.sum(axis=1, keepdims=True)
-        out[:, h, :] = p @ v[:, kv, :]
+    for r0 in range(0, m, rows_per_chunk):
+        r1 = min(m, r0 + rows_per_chunk)
+        qp = q_pos[r0:r1]
+        nk = int(qp.max()) + 1
+        mask = np.arange(nk)[None, :] > qp[:, None]
+        for h in range(Hq):
+            kv = h // group
+            s = (q[r0:r1, h, :] @ k[:nk, kv, :].T) / np.sqrt(hd)
+            s[mask] = -np.inf
+            s -= s.max(axis=1, keepdims=True)
+            np.exp(s, out=s)
+            s /= s.sum(axis=1, keepdims=True)
+            out[r0:r1, h, :] = s @ v[:nk, kv, :]
     return out
 
 
@@ -253,6 +260,8 @@ def silu(x: np.ndarray) -> np.ndarray:
 def _matmul_wT(shape, seed, layer, name, a, rnd: _Rounding, chunk_rows: int = 16384):
     """a @ W.T, W generated in row chunks to bound memory; fp32-rounded in the contract."""
     n_out, _ = tensor_dims(shape, name)
+    if a.shape[0] == 0:
+        return np.zeros((0, n_out))
     if n_out <= chunk_rows:
         return rnd.f32(a @ weight(shape, seed, layer, name).T)
     parts = []
@@ -263,17 +272,27 @@ def _matmul_wT(shape, seed, layer, name, a, rnd: _Rounding, chunk_rows: int = 16
 
 
 def forward(shape, seed: int, tokens: Sequence[int], rows: Sequence[int], mode: str = "contract",
-            return_kv: bool = False):
-    """Next-token logits at the given rows of `tokens`, computed from scratch.
+            return_kv: bool = False, past=None, trace=None):
+    """Next-token logits at the given rows of `tokens`.
+
+    Without `past` the tokens sit at positions 0..n-1 and everything is
+    computed from scratch.  With past = (ks, vs), the per-layer K and V of the
+    tokens at positions 0..p-1 as returned by an earlier call, the tokens sit
+    at positions p..p+n-1 and attend those cached keys and values before their
+    own (the same causal computation, with the earlier positions' K and V
+    taken from where they were first computed).
 
     Returns logits [len(rows)][V] (fp64 holding fp32 values in the contract
-    mode) and, if asked, the per-layer K and V caches [L][n][Hkv][hd] as the
-    GPU stores them (post-rotary, storage dtype)."""
+    mode) and, if asked, the per-layer K and V of `tokens` [L][n][Hkv][hd] as
+    the GPU stores them (post-rotary, storage form).  `trace`, if a dict,
+    receives each layer's stored intermediates (for tests of the rounding
+    contract)."""
     rnd = _Rounding(shape, mode)
     tokens = np.asarray(tokens, dtype=np.int64)
     n = len(tokens)
+    p0 = 0 if past is None else past[0].shape[1]
     Hq, Hkv, hd = shape.n_heads, shape.n_kv_heads, shape.head_dim
-    cos, sin = rope_table(shape, np.arange(n), rnd)
+    cos, sin = rope_table(shape, p0 + np.arange(n), rnd)
     h = embedding_rows(shape, seed, tokens)
     rows = np.asarray(rows, dtype=np.int64)
     ks, vs = [], []
@@ -293,20 +312,57 @@ def forward(shape, seed: int, tokens: Sequence[int], rows: Sequence[int], mode: 
         if return_kv:
             ks.append(k)
             vs.append(v)
-        att = rnd.operand(causal_attention(q, k, v, sel).reshape(len(sel), Hq * hd))
-        h = rnd.f32(h[sel] + _matmul_wT(shape, seed, l, "o", att, rnd))
+        kk = k if past is None else np.concatenate([past[0][l], k])
+        vv = v if past is None else np.concatenate([past[1][l], v])
+        att = rnd.operand(causal_attention(q, kk, vv, p0 + sel).reshape(len(sel), Hq * hd))
+        if trace is not None:
+            trace.setdefault("norm_in", []).append(a)
+            trace.setdefault("q", []).append(q)
+            trace.setdefault("k", []).append(k)
+            trace.setdefault("v", []).append(v)
+            trace.setdefault("att", []).append(att)
+        o = _matmul_wT(shape, seed, l, "o", att, rnd)
+        h = rnd.f32(h[sel] + o)
         a = rnd.operand(rms_norm(h, shape.rms_eps))
         g = _matmul_wT(shape, seed, l, "gate", a, rnd)
         u = _matmul_wT(shape, seed, l, "up", a, rnd)
         act = rnd.operand(silu(g) * u)
-        h = rnd.f32(h + _matmul_wT(shape, seed, l, "down", act, rnd))
+        dn = _matmul_wT(shape, seed, l, "down", act, rnd)
+        if trace is not None:
+            trace.setdefault("o_proj", []).append(o)
+            trace.setdefault("resid_mid", []).append(h)
+            trace.setdefault("ffn_in", []).append(a)
+            trace.setdefault("gate", []).append(g)
+            trace.setdefault("up", []).append(u)
+            trace.setdefault("act", []).append(act)
+            trace.setdefault("down", []).append(dn)
+        h = rnd.f32(h + dn)
+        if trace is not None:
+            trace.setdefault("resid", []).append(h)
     if shape.n_layers == 0:
         h = h[rows]
     a = rnd.operand(rms_norm(h, shape.rms_eps))
     logits = _matmul_wT(shape, seed, None, "lm_head", a, rnd)
+    if trace is not None:
+        trace["final_in"] = a
+        trace["logits"] = logits
     if return_kv:
         return logits, np.stack(ks), np.stack(vs)
     return logits
+
+
+def prefix_kv(shape, seed: int, tokens: Sequence[int], mode: str = "contract"):
+    """Per-layer K and V of `tokens` at positions 0..n-1 (the cache a verify
+    of the next block attends), computed from scratch."""
+    _, ks, vs = forward(shape, seed, tokens, [], mode, return_kv=True)
+    return ks, vs
+
+
+def extend_kv(past, ks, vs):
+    """past (K, V at positions 0..p-1) followed by K, V of the next tokens."""
+    if past is None:
+        return ks, vs
+    return np.concatenate([past[0], ks], axis=1), np.concatenate([past[1], vs], axis=1)
 
 
 # ---------------------------------------------------------------- the method
@@ -375,9 +431,11 @@ def decision_margins(z: np.ndarray, drafts: Sequence[int], n: int, tie_eps: floa
 
 def entropy(logits: np.ndarray) -> np.ndarray:
     """Shannon entropy in nats of softmax(logits) per row, fp64:
-    H = -sum_v p_v log p_v."""
+    H = -sum_v p_v log p_v, with 0 log 0 = 0 (ids whose logit is -inf)."""
     lp = log_softmax(logits)
-    return -(np.exp(lp) * lp).sum(-1)
+    p = np.exp(lp)
+    with np.errstate(invalid="ignore"):
+        return -np.where(p > 0, p * lp, 0.0).sum(-1)
 
 
 def accept_typical(z: np.ndarray, o: np.ndarray, drafts: Sequence[int], eps: float, delta: float,
@@ -499,19 +557,26 @@ def accept_sampling(z: np.ndarray, q: np.ndarray, drafts: Sequence[int], seed: i
 def verify(shape, seed: int, history: Sequence[int], drafts: Sequence[int], probe: Sequence[int],
            alpha: float, prefix_pos: int, mode: str = "contract", rule: str = "greedy", eps: float = 0.09,
            delta: float = 0.3, entropy_of: str = "fused", tie_eps: float = 1e-3, temperature: float = 1.0,
-           q: np.ndarray | None = None, rng_seed: int = 0, slot: int = 0) -> Dict:
+           q: np.ndarray | None = None, rng_seed: int = 0, slot: int = 0, past=None) -> Dict:
     """One verify step for one sequence: Algorithm 1's block with Algorithm
     2's rule (rule="greedy"), Algorithm 3's (rule="typical") or Algorithm 1's
     speculative sampling (rule="sampling", draft distributions q [k][V],
     random numbers from (rng_seed, batch slot `slot`)).  The fused logits are divided by
-    the temperature (fp32) before any rule."""
+    the temperature (fp32) before any rule.  `past`, if given, is
+    prefix_kv(history[:-1]): the block then attends it instead of the prefix
+    being recomputed."""
     history = [int(t) for t in history]
     drafts = [int(t) for t in drafts]
     block, shift, orig_rows, refl_rows = reflective_block(history, drafts, probe, prefix_pos)
     base = len(history) - 1
-    seq = history[:-1] + block
-    rows = [base + j for j in orig_rows] + [base + j for j in refl_rows]
-    logits = forward(shape, seed, seq, rows, mode)
+    if past is None:
+        seq = history[:-1] + block
+        rows = [base + j for j in orig_rows] + [base + j for j in refl_rows]
+        logits = forward(shape, seed, seq, rows, mode)
+    else:
+        if past[0].shape[1] != base:
+            raise ValueError("past must hold the K/V of history[:-1]")
+        logits = forward(shape, seed, block, orig_rows + refl_rows, mode, past=past)
     k = len(drafts)
     o, r = logits[: k + 1], logits[k + 1:]
     z = fuse(o, r, alpha)
@@ -537,12 +602,20 @@ def verify(shape, seed: int, history: Sequence[int], drafts: Sequence[int], prob
     }
 
 
-def greedy_continuation(shape, seed: int, history: Sequence[int], n_tokens: int, mode: str = "contract") -> List[int]:
-    """Target's own greedy continuation (used to build realistic drafts)."""
+def greedy_continuation(shape, seed: int, history: Sequence[int], n_tokens: int, mode: str = "contract",
+                        past=None) -> List[int]:
+    """Target's own greedy continuation (used to build realistic drafts).
+    Without `past` every token is recomputed from scratch over the whole
+    sequence; with past = prefix_kv(history[:-1]) each step runs one token on
+    top of the growing K/V of the earlier ones."""
     seq = [int(t) for t in history]
     out = []
     for _ in range(n_tokens):
-        logits = forward(shape, seed, seq, [len(seq) - 1], mode)
+        if past is None:
+            logits = forward(shape, seed, seq, [len(seq) - 1], mode)
+        else:
+            logits, ks, vs = forward(shape, seed, seq[-1:], [0], mode, return_kv=True, past=past)
+            past = extend_kv(past, ks, vs)
         t = int(np.argmax(logits[0]))
         out.append(t)
         seq.append(t)

@@ -119,7 +119,7 @@ RV_DEV Stat stat_of(const float (&x)[E], int n_valid) {
     if (e < n_valid) {
       const float d = x[e] - m, p = __expf(d);
       r.s += p;
-      r.s1 += p * d;
+      r.s1 += p > 0.f ? p * d : 0.f;  // 0 log 0 = 0 (ids at -inf)
     }
   return r;
 }
@@ -280,10 +280,16 @@ __global__ __launch_bounds__(512) void k_accept(HeadArgs a) {
       }
     }
   }
-  // any out-of-range id in the sequence's block (or its history) voids it
-  const int S = 1 + 2 * kb + a.n_probe + a.P, brow0 = b * (1 + a.n_probe + a.P) + 2 * Kb;
-  int badv = threadIdx.x == 0 ? a.seq_bad[b] : 0;
-  for (int j = threadIdx.x; j < S; j += blockDim.x) badv |= a.row_bad[brow0 + j];
+  // any out-of-range id in the sequence's block (or its history) voids it;
+  // without a block (logits given by the caller) the draft ids are checked
+  int badv = 0;
+  if (a.row_bad) {
+    const int S = 1 + 2 * kb + a.n_probe + a.P, brow0 = b * (1 + a.n_probe + a.P) + 2 * Kb;
+    if (threadIdx.x == 0) badv = a.seq_bad[b];
+    for (int j = threadIdx.x; j < S; j += blockDim.x) badv |= a.row_bad[brow0 + j];
+  } else {
+    for (int j = threadIdx.x; j < kb; j += blockDim.x) badv |= x[j] < 0 || x[j] >= a.V;
+  }
   const int bad = __syncthreads_or(badv);
   if (threadIdx.x != 0) return;
   float* mg = a.margins + (size_t)b * (a.k + 2);

@@ -10,8 +10,12 @@ namespace {
 // workgroup of d / (4 NPT) threads per row: every thread owns NPT float4s of
 // the row and issues all its loads (the gains, h and the pending k-group
 // partials of the previous matmul, added in k-group order) before using any
-// of them.  The updated h is written back after the workgroup's reduction
-// barrier, so the barrier does not wait for that store.
+// of them.  Without a gather the updated h is written back after the
+// workgroup's reduction barrier, so the barrier does not wait for that
+// store.  With a gather several output rows may read one source row (with no
+// probe and no prefix-position tokens, block row k feeds both o_{k+1} and
+// r_1), so h is only read: a write-back there would let a workgroup that
+// reads after another's store add the partials twice.
 // PB: partials loaded per batch, the smallest of 2, 4 and 8 that holds pk
 // (larger pk take several batches of 8); loads past pk repeat the last
 // partial and are not added.
@@ -55,7 +59,7 @@ __global__ __launch_bounds__(1024) void k_rmsnorm(float* __restrict__ h, int d, 
   float tot = 0.f;
   for (int w = 0; w < nw; ++w) tot += part[w];
   const float rs = 1.0f / sqrtf(tot / (float)d + eps);
-  if (P) {
+  if (P && !gather) {
 #pragma unroll
     for (int e = 0; e < NPT; ++e) *(f32x4_t*)(x + (threadIdx.x + e * blockDim.x) * 4) = v[e];
   }

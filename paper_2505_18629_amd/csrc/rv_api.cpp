@@ -819,6 +819,64 @@ rv_status rv_prefill_cache(rv_cache* c, const int32_t* d_prefix_ids, int32_t ld,
 
 namespace {
 
+// Arguments of the fusion / log-softmax / accept kernels over the cache's
+// logit rows (sequence b: its k_b+1 original rows, then its k_b+1 reflective
+// rows).  row_bad / seq_bad are left NULL (no block: draft ids are checked).
+HeadArgs head_args(rv_cache* c, int k, const uint8_t* kb, int R1, int n_probe, int P, const rv_fusion& fu,
+                   const float* d_q, uint64_t seed, const int32_t* d_draft_ids, const int32_t* h_prefix_len,
+                   int32_t* d_accept_len, int32_t* d_next_id) {
+  HeadArgs ha{};
+  ha.B = c->B;
+  ha.k = k;
+  ha.V = c->m->cfg.vocab;
+  ha.n_probe = n_probe;
+  ha.P = P;
+  ha.R1 = R1;
+  for (int b = 0; b < c->B; ++b) ha.kb[b] = kb[b];
+  ha.max_len = c->max_len;
+  ha.nchunk = c->nchunk;
+  ha.chunk = kVocabChunk;
+  ha.alpha = fu.alpha;
+  ha.rule = fu.rule;
+  ha.eps = fu.epsilon;
+  ha.delta = fu.delta;
+  ha.ent_src = fu.entropy_src;
+  ha.temp = fu.temperature;
+  ha.q = d_q;
+  ha.seed = seed;
+  ha.entropy = c->entropy;
+  ha.logits = c->logits;
+  ha.z = c->z;
+  ha.part = c->hpart;
+  ha.lse = c->lse;
+  ha.lp = c->lp;
+  ha.margins = c->margins;
+  ha.drafts = d_draft_ids;
+  ha.ids = c->ids;
+  ha.accept_len = d_accept_len;
+  ha.next_id = d_next_id;
+  ha.argmax = c->argmax;
+  for (int b = 0; b < c->B; ++b) ha.L[b] = h_prefix_len[b];
+  return ha;
+}
+
+// Validation of the fusion parameters shared by every verify entry point.
+rv_status check_fusion(const rv_fusion* fusion) {
+  if (!(fusion->temperature > 0.f && fusion->temperature < INFINITY))
+    return fail(RV_E_ARG, "temperature must be > 0 and finite");
+  if (!(fusion->alpha >= 0.f && fusion->alpha <= 1.f)) return fail(RV_E_ARG, "alpha must be in [0, 1]");
+  if (fusion->prefix_pos < 0) return fail(RV_E_ARG, "prefix_pos must be >= 0");
+  if (fusion->rule != RV_RULE_GREEDY && fusion->rule != RV_RULE_TYPICAL && fusion->rule != RV_RULE_SAMPLING)
+    return fail(RV_E_ARG, "unknown verification rule %d", fusion->rule);
+  if (fusion->rule == RV_RULE_TYPICAL) {
+    if (!(fusion->epsilon > 0.f)) return fail(RV_E_ARG, "epsilon must be > 0");
+    if (!(fusion->delta >= 0.f)) return fail(RV_E_ARG, "delta must be >= 0");
+    if (fusion->entropy_src != RV_ENTROPY_FUSED && fusion->entropy_src != RV_ENTROPY_ORIGINAL)
+      return fail(RV_E_ARG, "unknown entropy source %d", fusion->entropy_src);
+  }
+  return RV_OK;
+}
+
 // rv_verify and rv_verify_sampled: d_q / seed are used by the sampling rule only.
 // k is the draft-id stride and largest draft count; h_draft_len (may be NULL:
 // every sequence has k drafts) gives per-sequence counts.
@@ -832,22 +890,11 @@ rv_status verify_impl(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d
     return fail(RV_E_ARG, sampled ? "rv_verify_sampled needs rule RV_RULE_SAMPLING"
                                   : "the sampling rule needs the draft distributions (rv_verify_sampled)");
   if (sampled && k > 0 && !d_q) return fail(RV_E_ARG, "draft distributions are NULL");
-  if (!(fusion->temperature > 0.f && fusion->temperature < INFINITY))
-    return fail(RV_E_ARG, "temperature must be > 0 and finite");
   if (k < 0 || k > c->max_drafts) return fail(RV_E_ARG, "k = %d outside [0, max_drafts=%d]", k, c->max_drafts);
   if (k > 0 && !d_draft_ids) return fail(RV_E_ARG, "draft ids are NULL");
   if (n_probe < 0) return fail(RV_E_ARG, "n_probe must be >= 0");
   if (n_probe > 0 && !d_probe_ids) return fail(RV_E_ARG, "probe ids are NULL");
-  if (!(fusion->alpha >= 0.f && fusion->alpha <= 1.f)) return fail(RV_E_ARG, "alpha must be in [0, 1]");
-  if (fusion->prefix_pos < 0) return fail(RV_E_ARG, "prefix_pos must be >= 0");
-  if (fusion->rule != RV_RULE_GREEDY && fusion->rule != RV_RULE_TYPICAL && fusion->rule != RV_RULE_SAMPLING)
-    return fail(RV_E_ARG, "unknown verification rule %d", fusion->rule);
-  if (fusion->rule == RV_RULE_TYPICAL) {
-    if (!(fusion->epsilon > 0.f)) return fail(RV_E_ARG, "epsilon must be > 0");
-    if (!(fusion->delta >= 0.f)) return fail(RV_E_ARG, "delta must be >= 0");
-    if (fusion->entropy_src != RV_ENTROPY_FUSED && fusion->entropy_src != RV_ENTROPY_ORIGINAL)
-      return fail(RV_E_ARG, "unknown entropy source %d", fusion->entropy_src);
-  }
+  if (rv_status fs = check_fusion(fusion); fs != RV_OK) return fs;
   const int P = fusion->prefix_pos;
   uint8_t kb[RV_MAX_BATCH];
   int seg_end[RV_MAX_BATCH], seg_rows[RV_MAX_BATCH];
@@ -932,40 +979,10 @@ rv_status verify_impl(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d
     HIP_TRY(run_gemm(c, EPI_STORE, gl, false, st), "lm head");
   }
 
-  HeadArgs ha{};
-  ha.B = c->B;
-  ha.k = k;
-  ha.V = mc.vocab;
-  ha.n_probe = n_probe;
-  ha.P = P;
-  ha.R1 = R1;
-  for (int b = 0; b < c->B; ++b) ha.kb[b] = kb[b];
-  ha.max_len = c->max_len;
-  ha.nchunk = c->nchunk;
-  ha.chunk = kVocabChunk;
-  ha.alpha = fusion->alpha;
-  ha.rule = fusion->rule;
-  ha.eps = fusion->epsilon;
-  ha.delta = fusion->delta;
-  ha.ent_src = fusion->entropy_src;
-  ha.temp = fusion->temperature;
-  ha.q = d_q;
-  ha.seed = seed;
-  ha.entropy = c->entropy;
-  ha.logits = c->logits;
-  ha.z = c->z;
-  ha.part = c->hpart;
-  ha.lse = c->lse;
-  ha.lp = c->lp;
-  ha.margins = c->margins;
-  ha.drafts = d_draft_ids;
-  ha.ids = c->ids;
+  HeadArgs ha = head_args(c, k, kb, R1, n_probe, P, *fusion, d_q, seed, d_draft_ids, h_prefix_len, d_accept_len,
+                          d_next_id);
   ha.row_bad = c->row_bad;
   ha.seq_bad = c->seq_bad;
-  ha.accept_len = d_accept_len;
-  ha.next_id = d_next_id;
-  ha.argmax = c->argmax;
-  for (int b = 0; b < c->B; ++b) ha.L[b] = h_prefix_len[b];
   {
     Prof pf(c, RV_PROF_TAIL, st);
     HIP_TRY(launch_head(ha, st), "accept");
@@ -1001,6 +1018,34 @@ rv_status rv_verify_sampled(rv_cache* c, const int32_t* h_prefix_len, const int3
                             int32_t* d_next_id, void* stream) {
   return verify_impl(c, h_prefix_len, d_draft_ids, k, nullptr, d_draft_probs, d_probe_ids, n_probe, fusion, seed,
                      true, d_accept_len, d_next_id, stream);
+}
+
+rv_status rv_debug_fuse_accept(rv_cache* c, const float* d_logits, const int32_t* h_prefix_len,
+                               const int32_t* d_draft_ids, int32_t k, const rv_fusion* fusion, int32_t* d_accept_len,
+                               int32_t* d_next_id, void* stream) {
+  if (!c || !d_logits || !h_prefix_len || !fusion || !d_accept_len || !d_next_id)
+    return fail(RV_E_ARG, "cache, logits, prefix_len, fusion and outputs must not be NULL");
+  if (k < 0 || k > c->max_drafts) return fail(RV_E_ARG, "k = %d outside [0, max_drafts=%d]", k, c->max_drafts);
+  if (k > 0 && !d_draft_ids) return fail(RV_E_ARG, "draft ids are NULL");
+  if (rv_status fs = check_fusion(fusion); fs != RV_OK) return fs;
+  if (fusion->rule == RV_RULE_SAMPLING) return fail(RV_E_ARG, "the sampling rule is not available here");
+  for (int b = 0; b < c->B; ++b) {
+    const int L = h_prefix_len[b];
+    if (L < 1 || (long long)L + k + 1 > c->max_len)
+      return fail(RV_E_RANGE, "prefix_len[%d] = %d: needs 1 <= L and L + k + 1 <= max_len=%d", b, L, c->max_len);
+  }
+  uint8_t kb[RV_MAX_BATCH];
+  for (int b = 0; b < c->B; ++b) kb[b] = (uint8_t)k;
+  const int R1 = c->B * (k + 1);
+  hipStream_t st = (hipStream_t)stream;
+  HIP_TRY(hipMemcpyAsync(c->logits, d_logits, (size_t)2 * R1 * c->m->cfg.vocab * 4, hipMemcpyDeviceToDevice, st),
+          "copy logits");
+  HeadArgs ha = head_args(c, k, kb, R1, 0, 0, *fusion, nullptr, 0, d_draft_ids, h_prefix_len, d_accept_len, d_next_id);
+  HIP_TRY(launch_head(ha, st), "accept");
+  c->last_k = k;
+  c->last_R1 = R1;
+  for (int b = 0; b < c->B; ++b) c->last_kb[b] = kb[b];
+  return RV_OK;
 }
 
 rv_status rv_debug_output(const rv_cache* c, int32_t which, float* d_dst, size_t dst_bytes, void* stream) {

@@ -101,8 +101,9 @@ hipError_t launch_export_kv(const void* src_hi, const void* src_lo, int hd, int 
 // RMSNorm of rows of the fp32 residual h into matmul operands (out, out2).  Output row r
 // reads source row gather[r] (gather != NULL: the rows the LM head needs) or r.
 // With P != NULL the source row first takes h += sum over g < gk of P[g][row]
-// (k-group order; P holds p_rows rows per k-group) and writes h back (the
-// pending partials of the previous matmul).
+// (k-group order; P holds p_rows rows per k-group): the pending partials of
+// the previous matmul.  Without a gather h is written back; with one it is
+// only read (output rows may share a source row).
 hipError_t launch_rmsnorm(int dtype, float* h, int rows, int d, const float* gain, float eps, void* out,
                           void* out2, const int* gather, const float* P, int gk, int p_rows, hipStream_t st);
 
@@ -201,8 +202,8 @@ struct HeadArgs {
   float* margins;        // [B][k+2]: margins of tested drafts, then top1-top2 gap last
   const int* drafts;     // [B][k]
   int* ids;              // history [B][max_len]
-  const int* row_bad;    // [block rows]
-  const int* seq_bad;    // [B]
+  const int* row_bad;    // [block rows], or NULL: logits given by the caller (draft ids checked instead)
+  const int* seq_bad;    // [B] (with row_bad)
   int* accept_len;
   int* next_id;
   int* argmax;           // [R1]

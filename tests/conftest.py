@@ -16,8 +16,8 @@ def pytest_configure(config):
 def _ensure_built():
     lib = os.path.join(ROOT, "paper_2505_18629_amd", "librv.so")
     if not os.path.exists(lib):
-        from paper_2505_18629_amd.build import build
-        build()
+        from __graft_entry__ import _build_script
+        _build_script().build()
     orc = os.path.join(ROOT, "oracle", "liboracle_weights.so")
     if not os.path.exists(orc):
         import oracle

@@ -164,6 +164,12 @@ def test_entropy_closed_forms():
     x = rng.standard_normal((6, 50)) * 2
     ref = scipy.stats.entropy(scipy.special.softmax(x, axis=-1), axis=-1)
     np.testing.assert_allclose(oracle.entropy(x), ref, rtol=1e-12)
+    # ids at -inf have probability 0 and add nothing (0 log 0 = 0): the
+    # entropy is that of the row without them
+    xm = x.copy()
+    xm[:, ::3] = -np.inf
+    ref = scipy.stats.entropy(scipy.special.softmax(x[:, [j for j in range(50) if j % 3]], axis=-1), axis=-1)
+    np.testing.assert_allclose(oracle.entropy(xm), ref, rtol=1e-12)
 
 
 def test_typical_monotone_and_end_points():
