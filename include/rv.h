@@ -243,11 +243,14 @@ rv_status rv_debug_fuse_accept(rv_cache* c, const float* d_logits, const int32_t
  * its decision from the boundary (greedy: z_i[x_i] - max_{v != x_i} z_i[v];
  * typical: log p_i(x_i) - log threshold_i; sampling: log p_i(x_i) -
  * log(r_i q_i(x_i)); NaN for untested drafts), NaN, and last the top-1
- * minus top-2 gap of z_{n+1} (sampling: of the perturbed draw scores). */
+ * minus top-2 gap of z_{n+1} (sampling: of the perturbed draw scores).
+ * RV_OUT_PROB_FUSED is the fused distribution p_i = softmax(z_i) itself
+ * (exp of RV_OUT_LOGP_FUSED), e.g. the draft distributions q_i a sampling
+ * draft model hands to rv_verify_sampled. */
 enum {
   RV_OUT_ORIG = 0, RV_OUT_REFL = 1, RV_OUT_FUSED = 2,
   RV_OUT_LOGP_ORIG = 3, RV_OUT_LOGP_REFL = 4, RV_OUT_LOGP_FUSED = 5,
-  RV_OUT_ENTROPY = 6, RV_OUT_MARGINS = 7
+  RV_OUT_ENTROPY = 6, RV_OUT_MARGINS = 7, RV_OUT_PROB_FUSED = 8
 };
 
 /* Copies one result of the last verify into d_dst (at least the byte size

@@ -32,7 +32,7 @@ RV_RULE_GREEDY, RV_RULE_TYPICAL, RV_RULE_SAMPLING = 0, 1, 2
 RV_ENTROPY_FUSED, RV_ENTROPY_ORIGINAL = 0, 1
 RV_MAX_BATCH, RV_MAX_DRAFTS = 256, 32
 (RV_OUT_ORIG, RV_OUT_REFL, RV_OUT_FUSED, RV_OUT_LOGP_ORIG, RV_OUT_LOGP_REFL, RV_OUT_LOGP_FUSED, RV_OUT_ENTROPY,
- RV_OUT_MARGINS) = range(8)
+ RV_OUT_MARGINS, RV_OUT_PROB_FUSED) = range(9)
 RV_MAT_QKV, RV_MAT_O, RV_MAT_GATEUP, RV_MAT_DOWN, RV_MAT_LM_HEAD = range(5)
 RV_WS_RESID, RV_WS_ATTN, RV_WS_ACT, RV_WS_QUERY = range(4)
 PROF_CLASSES = ["plan", "norm", "qkv", "attn", "combine", "o", "gateup", "down", "lmhead", "tail"]
@@ -41,7 +41,8 @@ STATUS = {0: "RV_OK", -1: "RV_E_ARG", -2: "RV_E_RANGE", -3: "RV_E_CAPACITY", -4:
 
 EXPORTED = [
     "rv_status_str", "rv_last_error", "rv_model_bytes", "rv_init_weights", "rv_model_free",
-    "rv_cache_bytes", "rv_cache_create", "rv_cache_free", "rv_prefill_cache", "rv_verify", "rv_verify_sampled", "rv_verify_ragged", "rv_commit_tokens",
+    "rv_cache_bytes", "rv_cache_create", "rv_cache_free", "rv_prefill_cache", "rv_verify", "rv_verify_sampled",
+    "rv_verify_ragged", "rv_commit_tokens",
     "rv_debug_fuse_accept", "rv_debug_output", "rv_debug_export_kv", "rv_debug_export_ids", "rv_debug_weight_bits",
     "rv_debug_linear", "rv_debug_workspace", "rv_debug_profile", "rv_debug_profile_read", "rv_debug_time_matrix",
 ]

@@ -211,9 +211,10 @@ __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
   }
 }
 
-// One 256-thread workgroup per sequence.  Wave w merges the chunk statistics
-// of fused rows w, w+4, ...: lane c takes chunks c and c+64, then the wave
-// merges lanes in a fixed butterfly order.  Thread 0 then applies the rule.
+// One 512-thread workgroup (8 waves) per sequence.  Wave w merges the chunk
+// statistics of fused rows w, w+8, ...: lane c takes chunks c and c+64, then
+// the wave merges lanes in a fixed butterfly order.  Thread 0 then applies
+// the rule.
 __global__ __launch_bounds__(512) void k_accept(HeadArgs a) {
   const int b = blockIdx.x, lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int kb = a.kb[b], k1 = kb + 1, R1 = a.R1, Kb = kb_prefix(a.kb, b);
@@ -461,7 +462,19 @@ __global__ __launch_bounds__(256) void k_logprob(HeadArgs a) {
   }
 }
 
+// dst[i] = exp(src[i]): probabilities from log-probabilities.
+__global__ __launch_bounds__(256) void k_exp(const float* __restrict__ src, float* __restrict__ dst, size_t n) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) dst[i] = expf(src[i]);
+}
+
 }  // namespace
+
+hipError_t launch_exp(const float* src, float* dst, size_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  k_exp<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(src, dst, n);
+  return hipGetLastError();
+}
 
 hipError_t launch_head(const HeadArgs& a, hipStream_t st) {
   const int R1 = a.R1;

@@ -13,7 +13,9 @@ namespace {
 
 thread_local std::string g_err;
 
-rv_status fail(rv_status s, const char* fmt, ...) {
+}  // namespace
+
+rv_status rv_fail(rv_status s, const char* fmt, ...) {
   char buf[512];
   va_list ap;
   va_start(ap, fmt);
@@ -23,8 +25,11 @@ rv_status fail(rv_status s, const char* fmt, ...) {
   return s;
 }
 
+namespace {
+
+
 rv_status hip_fail(hipError_t e, const char* what) {
-  return fail(RV_E_HIP, "%s: %s", what, hipGetErrorString(e));
+  return rv_fail(RV_E_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
 #define HIP_TRY(expr, what)                 \
@@ -34,8 +39,6 @@ rv_status hip_fail(hipError_t e, const char* what) {
   } while (0)
 
 constexpr size_t kAlign = 256;
-constexpr int kPrefillRows = 2048;   // rows per prefill chunk
-constexpr int kSplitsPerQuery = 8;   // partial-buffer depth per query row
 constexpr int kVocabChunk = 2048;    // vocabulary chunk of the LM-head tail (8 entries per thread)
 constexpr int kMaxSplitK = 16;       // k-groups of a split matmul
 constexpr int kMaxSplitTiled = 4;    // k-groups of a split many-token matmul
@@ -123,21 +126,21 @@ struct rv_cache {
 namespace {
 
 rv_status check_config(const rv_config* c) {
-  if (!c) return fail(RV_E_ARG, "config is NULL");
-  if (c->dtype != RV_F32 && c->dtype != RV_BF16) return fail(RV_E_ARG, "dtype must be RV_F32 or RV_BF16");
+  if (!c) return rv_fail(RV_E_ARG, "config is NULL");
+  if (c->dtype != RV_F32 && c->dtype != RV_BF16) return rv_fail(RV_E_ARG, "dtype must be RV_F32 or RV_BF16");
   if (c->n_layers <= 0 || c->d_model <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 || c->ffn_dim <= 0 ||
       c->vocab <= 0)
-    return fail(RV_E_ARG, "shape fields must be positive");
-  if (c->vocab > 64 * 2 * 2048) return fail(RV_E_ARG, "vocab must be <= 262144");
+    return rv_fail(RV_E_ARG, "shape fields must be positive");
+  if (c->vocab > 64 * 2 * 2048) return rv_fail(RV_E_ARG, "vocab must be <= 262144");
   if (c->d_model % 128 || c->ffn_dim % 128 || (c->n_heads * c->head_dim) % 128)
-    return fail(RV_E_ARG, "d_model, ffn_dim and n_heads*head_dim must be multiples of 128");
+    return rv_fail(RV_E_ARG, "d_model, ffn_dim and n_heads*head_dim must be multiples of 128");
   if (c->head_dim != 32 && c->head_dim != 64 && c->head_dim != 128)
-    return fail(RV_E_ARG, "head_dim must be 32, 64 or 128");
-  if (c->n_heads % c->n_kv_heads) return fail(RV_E_ARG, "n_heads must be a multiple of n_kv_heads");
-  if (c->vocab % 16) return fail(RV_E_ARG, "vocab must be a multiple of 16");
-  if ((long long)c->vocab * c->d_model >= (1LL << 36)) return fail(RV_E_ARG, "tensor too large for the generator");
+    return rv_fail(RV_E_ARG, "head_dim must be 32, 64 or 128");
+  if (c->n_heads % c->n_kv_heads) return rv_fail(RV_E_ARG, "n_heads must be a multiple of n_kv_heads");
+  if (c->vocab % 16) return rv_fail(RV_E_ARG, "vocab must be a multiple of 16");
+  if ((long long)c->vocab * c->d_model >= (1LL << 36)) return rv_fail(RV_E_ARG, "tensor too large for the generator");
   if (!(c->rms_eps > 0.f) || !(c->rope_base > 1.f) || !(c->init_std > 0.f))
-    return fail(RV_E_ARG, "rms_eps, init_std must be > 0 and rope_base > 1");
+    return rv_fail(RV_E_ARG, "rms_eps, init_std must be > 0 and rope_base > 1");
   return RV_OK;
 }
 
@@ -181,13 +184,13 @@ size_t cache_layout(rv_cache* c, void* buf) {
   const rv_config& mc = c->m->cfg;
   const int es = c->m->es, d = mc.d_model, hd = mc.head_dim;
   const int qd = mc.n_heads * hd;
-  c->rows_cap = round_up(std::max(c->B * c->max_block, kPrefillRows), 64);
+  c->rows_cap = cache_rows_cap(c->B, c->max_block);
   c->out_rows_cap = round_up(c->B * 2 * (c->max_drafts + 1), 64);
   c->r1_cap = c->B * (c->max_drafts + 1);
   c->nchunk = (mc.vocab + kVocabChunk - 1) / kVocabChunk;
   c->kv_len = round_up(c->max_len, 64);
   c->kv_layer_elems = (size_t)c->B * mc.n_kv_heads * c->kv_len * hd;
-  c->part_entries = (size_t)c->rows_cap * mc.n_heads * kSplitsPerQuery;
+  c->part_entries = cache_part_entries(c->rows_cap, mc.n_heads);
   const int nseg_cap = std::max(c->B, (int)RV_MAX_SEGS);
   Carve cv(buf);
   // bf16 models keep K and V as hi/lo bf16 planes (the operand form)
@@ -410,28 +413,10 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, c
   const int qmax = G * max_seg_rows;
   const int groups = nseg * mc.n_kv_heads;
   const int qgroups = (qmax + 127) / 128;
-  // Key split (a multiple of 64 keys): minimise the estimated attention time,
-  // rounds of 256 workgroups (one per CU) x (64-key tiles per workgroup + a
-  // per-workgroup overhead of about two tiles), counting the workgroups that
-  // have keys (segment s has keys 0 .. h_seg_end[s]-1); bounded by the
-  // partial buffer and by the combine kernel's 64 splits per query.  (70B
-  // batch 8 at 8K context: 4 splits, 768 workgroups, 348 us per layer vs
-  // 393 us with 3 splits and 576.)
-  int ks = 0;
-  double best = 0;
-  for (int cand = 64; cand <= round_up(kmax, 64); cand += 64) {
-    const int ns = (kmax + cand - 1) / cand;
-    if (ns > 64 || (size_t)ns * groups * qmax > c->part_entries) continue;
-    long long wgs = 0;
-    for (int s = 0; s < nseg; ++s)
-      wgs += (long long)((h_seg_end[s] + cand - 1) / cand) * mc.n_kv_heads * ((G * h_seg_rows[s] + 127) / 128);
-    const double t = (double)((wgs + 255) / 256) * (cand / 64 + 2);
-    if (ks == 0 || t < best) {
-      best = t;
-      ks = cand;
-    }
-  }
-  if (ks == 0) return fail(RV_E_CAPACITY, "attention partial buffer too small for %d keys", kmax);
+  // Key split (plan_attn_split; 70B batch 8 at 8K context: 4 splits, 768
+  // workgroups, 348 us per layer vs 393 us with 3 splits and 576).
+  const int ks = plan_attn_split(kmax, nseg, h_seg_end, h_seg_rows, mc.n_kv_heads, G, qmax, c->part_entries);
+  if (ks == 0) return rv_fail(RV_E_CAPACITY, "attention partial buffer too small for %d keys", kmax);
   const int nsplit = (kmax + ks - 1) / ks;
 
   AttnArgs at{};
@@ -619,7 +604,7 @@ const char* rv_last_error(void) { return g_err.c_str(); }
 rv_status rv_model_bytes(const rv_config* cfg, size_t* bytes) {
   rv_status s = check_config(cfg);
   if (s != RV_OK) return s;
-  if (!bytes) return fail(RV_E_ARG, "bytes is NULL");
+  if (!bytes) return rv_fail(RV_E_ARG, "bytes is NULL");
   rv_model m{};
   m.cfg = *cfg;
   m.es = cfg->dtype == RV_BF16 ? 2 : 4;
@@ -632,7 +617,7 @@ rv_status rv_init_weights(const rv_config* cfg, uint64_t seed, void* d_buf, size
                           rv_model** out) {
   rv_status s = check_config(cfg);
   if (s != RV_OK) return s;
-  if (!d_buf || !out) return fail(RV_E_ARG, "d_buf and out must not be NULL");
+  if (!d_buf || !out) return rv_fail(RV_E_ARG, "d_buf and out must not be NULL");
   rv_model* m = new rv_model();
   m->cfg = *cfg;
   m->seed = seed;
@@ -641,7 +626,7 @@ rv_status rv_init_weights(const rv_config* cfg, uint64_t seed, void* d_buf, size
   size_t need = model_layout(m, nullptr);
   if (buf_bytes < need) {
     delete m;
-    return fail(RV_E_BUFFER, "model buffer has %zu bytes, needs %zu", buf_bytes, need);
+    return rv_fail(RV_E_BUFFER, "model buffer has %zu bytes, needs %zu", buf_bytes, need);
   }
   m->base = (char*)d_buf;
   m->bytes = need;
@@ -685,10 +670,10 @@ void rv_model_free(rv_model* m) { delete m; }
 
 rv_status rv_cache_bytes(const rv_model* m, int32_t batch, int32_t max_len, int32_t max_block, int32_t max_drafts,
                          size_t* bytes) {
-  if (!m || !bytes) return fail(RV_E_ARG, "model and bytes must not be NULL");
-  if (batch <= 0 || batch > RV_MAX_BATCH) return fail(RV_E_ARG, "batch must be in [1, %d]", RV_MAX_BATCH);
+  if (!m || !bytes) return rv_fail(RV_E_ARG, "model and bytes must not be NULL");
+  if (batch <= 0 || batch > RV_MAX_BATCH) return rv_fail(RV_E_ARG, "batch must be in [1, %d]", RV_MAX_BATCH);
   if (max_len <= 0 || max_block <= 0 || max_drafts < 0 || max_drafts > RV_MAX_DRAFTS)
-    return fail(RV_E_ARG, "max_len, max_block must be > 0 and max_drafts in [0, %d]", RV_MAX_DRAFTS);
+    return rv_fail(RV_E_ARG, "max_len, max_block must be > 0 and max_drafts in [0, %d]", RV_MAX_DRAFTS);
   rv_cache c{};
   c.m = const_cast<rv_model*>(m);
   c.B = batch;
@@ -704,8 +689,8 @@ rv_status rv_cache_create(rv_model* m, int32_t batch, int32_t max_len, int32_t m
   size_t need = 0;
   rv_status s = rv_cache_bytes(m, batch, max_len, max_block, max_drafts, &need);
   if (s != RV_OK) return s;
-  if (!d_buf || !out) return fail(RV_E_ARG, "d_buf and out must not be NULL");
-  if (buf_bytes < need) return fail(RV_E_BUFFER, "cache buffer has %zu bytes, needs %zu", buf_bytes, need);
+  if (!d_buf || !out) return rv_fail(RV_E_ARG, "d_buf and out must not be NULL");
+  if (buf_bytes < need) return rv_fail(RV_E_BUFFER, "cache buffer has %zu bytes, needs %zu", buf_bytes, need);
   rv_cache* c = new rv_cache();
   c->m = m;
   c->B = batch;
@@ -740,12 +725,12 @@ void rv_cache_free(rv_cache* c) { delete c; }
 
 rv_status rv_prefill_cache(rv_cache* c, const int32_t* d_prefix_ids, int32_t ld, const int32_t* h_prefix_len,
                            void* stream) {
-  if (!c || !d_prefix_ids || !h_prefix_len) return fail(RV_E_ARG, "cache, ids and lengths must not be NULL");
-  if (ld <= 0) return fail(RV_E_ARG, "ld must be positive");
+  if (!c || !d_prefix_ids || !h_prefix_len) return rv_fail(RV_E_ARG, "cache, ids and lengths must not be NULL");
+  if (ld <= 0) return rv_fail(RV_E_ARG, "ld must be positive");
   for (int b = 0; b < c->B; ++b) {
     const int L = h_prefix_len[b];
     if (L < 1 || L > c->max_len || L > ld)
-      return fail(RV_E_RANGE, "prefix_len[%d] = %d outside [1, min(max_len=%d, ld=%d)]", b, L, c->max_len, ld);
+      return rv_fail(RV_E_RANGE, "prefix_len[%d] = %d outside [1, min(max_len=%d, ld=%d)]", b, L, c->max_len, ld);
   }
   hipStream_t st = (hipStream_t)stream;
   const rv_config& mc = c->m->cfg;
@@ -775,40 +760,21 @@ rv_status rv_prefill_cache(rv_cache* c, const int32_t* d_prefix_ids, int32_t ld,
   pp.seg_n = c->seg_n;
   pp.seg_pos0 = c->seg_pos0;
   int b = 0, pos = 0;
-  while (true) {
-    while (b < c->B && pos >= h_prefix_len[b] - 1) {
-      ++b;
-      pos = 0;
-    }
-    if (b >= c->B) break;
-    int rows = 0, nseg = 0, max_n = 0, kmax = 0;
-    while (b < c->B && rows < c->rows_cap && nseg < RV_MAX_SEGS) {
-      const int avail = h_prefix_len[b] - 1 - pos;
-      if (avail <= 0) {
-        ++b;
-        pos = 0;
-        continue;
-      }
-      const int n = std::min(avail, c->rows_cap - rows);
-      pp.sb[nseg] = b;
-      pp.spos0[nseg] = pos;
-      pp.sn[nseg] = n;
-      pp.srow0[nseg] = rows;
-      ++nseg;
-      rows += n;
-      pos += n;
-      max_n = std::max(max_n, n);
-      kmax = std::max(kmax, pos);
-    }
-    pp.nseg = nseg;
-    pp.rows = rows;
+  PrefillChunk ch;
+  while (next_prefill_chunk(h_prefix_len, c->B, c->rows_cap, b, pos, ch)) {
+    pp.nseg = ch.nseg;
+    pp.rows = ch.rows;
+    std::copy(ch.sb, ch.sb + ch.nseg, pp.sb);
+    std::copy(ch.spos0, ch.spos0 + ch.nseg, pp.spos0);
+    std::copy(ch.sn, ch.sn + ch.nseg, pp.sn);
+    std::copy(ch.srow0, ch.srow0 + ch.nseg, pp.srow0);
     {
       Prof pf(c, RV_PROF_PLAN, st);
       HIP_TRY(launch_plan_prefill(mc.dtype, pp, st), "prefill plan");
     }
     int seg_end[RV_MAX_SEGS];
-    for (int i = 0; i < nseg; ++i) seg_end[i] = pp.spos0[i] + pp.sn[i];
-    rv_status s = run_layers(c, rows, nseg, max_n, kmax, seg_end, pp.sn, false, nullptr, st);
+    for (int i = 0; i < ch.nseg; ++i) seg_end[i] = ch.spos0[i] + ch.sn[i];
+    rv_status s = run_layers(c, ch.rows, ch.nseg, ch.max_n, ch.kmax, seg_end, ch.sn, false, nullptr, st);
     if (s != RV_OK) return s;
   }
   c->last_k = -1;
@@ -860,22 +826,25 @@ HeadArgs head_args(rv_cache* c, int k, const uint8_t* kb, int R1, int n_probe, i
   return ha;
 }
 
-// Validation of the fusion parameters shared by every verify entry point.
-rv_status check_fusion(const rv_fusion* fusion) {
+}  // namespace
+
+rv_status rv_check_fusion(const rv_fusion* fusion) {
   if (!(fusion->temperature > 0.f && fusion->temperature < INFINITY))
-    return fail(RV_E_ARG, "temperature must be > 0 and finite");
-  if (!(fusion->alpha >= 0.f && fusion->alpha <= 1.f)) return fail(RV_E_ARG, "alpha must be in [0, 1]");
-  if (fusion->prefix_pos < 0) return fail(RV_E_ARG, "prefix_pos must be >= 0");
+    return rv_fail(RV_E_ARG, "temperature must be > 0 and finite");
+  if (!(fusion->alpha >= 0.f && fusion->alpha <= 1.f)) return rv_fail(RV_E_ARG, "alpha must be in [0, 1]");
+  if (fusion->prefix_pos < 0) return rv_fail(RV_E_ARG, "prefix_pos must be >= 0");
   if (fusion->rule != RV_RULE_GREEDY && fusion->rule != RV_RULE_TYPICAL && fusion->rule != RV_RULE_SAMPLING)
-    return fail(RV_E_ARG, "unknown verification rule %d", fusion->rule);
+    return rv_fail(RV_E_ARG, "unknown verification rule %d", fusion->rule);
   if (fusion->rule == RV_RULE_TYPICAL) {
-    if (!(fusion->epsilon > 0.f)) return fail(RV_E_ARG, "epsilon must be > 0");
-    if (!(fusion->delta >= 0.f)) return fail(RV_E_ARG, "delta must be >= 0");
+    if (!(fusion->epsilon > 0.f)) return rv_fail(RV_E_ARG, "epsilon must be > 0");
+    if (!(fusion->delta >= 0.f)) return rv_fail(RV_E_ARG, "delta must be >= 0");
     if (fusion->entropy_src != RV_ENTROPY_FUSED && fusion->entropy_src != RV_ENTROPY_ORIGINAL)
-      return fail(RV_E_ARG, "unknown entropy source %d", fusion->entropy_src);
+      return rv_fail(RV_E_ARG, "unknown entropy source %d", fusion->entropy_src);
   }
   return RV_OK;
 }
+
+namespace {
 
 // rv_verify and rv_verify_sampled: d_q / seed are used by the sampling rule only.
 // k is the draft-id stride and largest draft count; h_draft_len (may be NULL:
@@ -885,32 +854,32 @@ rv_status verify_impl(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d
                       const rv_fusion* fusion, uint64_t seed, bool sampled, int32_t* d_accept_len,
                       int32_t* d_next_id, void* stream) {
   if (!c || !h_prefix_len || !fusion || !d_accept_len || !d_next_id)
-    return fail(RV_E_ARG, "cache, prefix_len, fusion and outputs must not be NULL");
+    return rv_fail(RV_E_ARG, "cache, prefix_len, fusion and outputs must not be NULL");
   if (sampled != (fusion->rule == RV_RULE_SAMPLING))
-    return fail(RV_E_ARG, sampled ? "rv_verify_sampled needs rule RV_RULE_SAMPLING"
+    return rv_fail(RV_E_ARG, sampled ? "rv_verify_sampled needs rule RV_RULE_SAMPLING"
                                   : "the sampling rule needs the draft distributions (rv_verify_sampled)");
-  if (sampled && k > 0 && !d_q) return fail(RV_E_ARG, "draft distributions are NULL");
-  if (k < 0 || k > c->max_drafts) return fail(RV_E_ARG, "k = %d outside [0, max_drafts=%d]", k, c->max_drafts);
-  if (k > 0 && !d_draft_ids) return fail(RV_E_ARG, "draft ids are NULL");
-  if (n_probe < 0) return fail(RV_E_ARG, "n_probe must be >= 0");
-  if (n_probe > 0 && !d_probe_ids) return fail(RV_E_ARG, "probe ids are NULL");
-  if (rv_status fs = check_fusion(fusion); fs != RV_OK) return fs;
+  if (sampled && k > 0 && !d_q) return rv_fail(RV_E_ARG, "draft distributions are NULL");
+  if (k < 0 || k > c->max_drafts) return rv_fail(RV_E_ARG, "k = %d outside [0, max_drafts=%d]", k, c->max_drafts);
+  if (k > 0 && !d_draft_ids) return rv_fail(RV_E_ARG, "draft ids are NULL");
+  if (n_probe < 0) return rv_fail(RV_E_ARG, "n_probe must be >= 0");
+  if (n_probe > 0 && !d_probe_ids) return rv_fail(RV_E_ARG, "probe ids are NULL");
+  if (rv_status fs = rv_check_fusion(fusion); fs != RV_OK) return fs;
   const int P = fusion->prefix_pos;
   uint8_t kb[RV_MAX_BATCH];
   int seg_end[RV_MAX_BATCH], seg_rows[RV_MAX_BATCH];
   int S_max = 0, M = 0, R1 = 0, kmax = 0;
   for (int b = 0; b < c->B; ++b) {
     const int kk = h_draft_len ? h_draft_len[b] : k;
-    if (kk < 0 || kk > k) return fail(RV_E_ARG, "draft count %d of sequence %d outside [0, %d]", kk, b, k);
+    if (kk < 0 || kk > k) return rv_fail(RV_E_ARG, "draft count %d of sequence %d outside [0, %d]", kk, b, k);
     kb[b] = (uint8_t)kk;
     const long long S = 1LL + 2LL * kk + n_probe + P;
-    if (S > c->max_block) return fail(RV_E_CAPACITY, "block of %lld rows exceeds max_block=%d", S, c->max_block);
+    if (S > c->max_block) return rv_fail(RV_E_CAPACITY, "block of %lld rows exceeds max_block=%d", S, c->max_block);
     const int L = h_prefix_len[b];
     if (L < std::max(1, P) || L > c->max_len)
-      return fail(RV_E_RANGE, "prefix_len[%d] = %d outside [max(1, P)=%d, max_len=%d]", b, L, std::max(1, P),
+      return rv_fail(RV_E_RANGE, "prefix_len[%d] = %d outside [max(1, P)=%d, max_len=%d]", b, L, std::max(1, P),
                   c->max_len);
     if ((long long)L - 1 + S > c->max_len || (long long)L + kk + 1 > c->max_len)
-      return fail(RV_E_CAPACITY, "sequence %d: block of %lld rows at length %d exceeds max_len=%d", b, S, L,
+      return rv_fail(RV_E_CAPACITY, "sequence %d: block of %lld rows at length %d exceeds max_len=%d", b, S, L,
                   c->max_len);
     kmax = std::max(kmax, (int)(L - 1 + S));
     seg_end[b] = (int)(L - 1 + S);
@@ -1007,7 +976,7 @@ rv_status rv_verify(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_d
 rv_status rv_verify_ragged(rv_cache* c, const int32_t* h_prefix_len, const int32_t* d_draft_ids, int32_t ld_drafts,
                            const int32_t* h_draft_len, const int32_t* d_probe_ids, int32_t n_probe,
                            const rv_fusion* fusion, int32_t* d_accept_len, int32_t* d_next_id, void* stream) {
-  if (!h_draft_len) return fail(RV_E_ARG, "draft lengths must not be NULL");
+  if (!h_draft_len) return rv_fail(RV_E_ARG, "draft lengths must not be NULL");
   return verify_impl(c, h_prefix_len, d_draft_ids, ld_drafts, h_draft_len, nullptr, d_probe_ids, n_probe, fusion, 0,
                      false, d_accept_len, d_next_id, stream);
 }
@@ -1024,15 +993,15 @@ rv_status rv_debug_fuse_accept(rv_cache* c, const float* d_logits, const int32_t
                                const int32_t* d_draft_ids, int32_t k, const rv_fusion* fusion, int32_t* d_accept_len,
                                int32_t* d_next_id, void* stream) {
   if (!c || !d_logits || !h_prefix_len || !fusion || !d_accept_len || !d_next_id)
-    return fail(RV_E_ARG, "cache, logits, prefix_len, fusion and outputs must not be NULL");
-  if (k < 0 || k > c->max_drafts) return fail(RV_E_ARG, "k = %d outside [0, max_drafts=%d]", k, c->max_drafts);
-  if (k > 0 && !d_draft_ids) return fail(RV_E_ARG, "draft ids are NULL");
-  if (rv_status fs = check_fusion(fusion); fs != RV_OK) return fs;
-  if (fusion->rule == RV_RULE_SAMPLING) return fail(RV_E_ARG, "the sampling rule is not available here");
+    return rv_fail(RV_E_ARG, "cache, logits, prefix_len, fusion and outputs must not be NULL");
+  if (k < 0 || k > c->max_drafts) return rv_fail(RV_E_ARG, "k = %d outside [0, max_drafts=%d]", k, c->max_drafts);
+  if (k > 0 && !d_draft_ids) return rv_fail(RV_E_ARG, "draft ids are NULL");
+  if (rv_status fs = rv_check_fusion(fusion); fs != RV_OK) return fs;
+  if (fusion->rule == RV_RULE_SAMPLING) return rv_fail(RV_E_ARG, "the sampling rule is not available here");
   for (int b = 0; b < c->B; ++b) {
     const int L = h_prefix_len[b];
     if (L < 1 || (long long)L + k + 1 > c->max_len)
-      return fail(RV_E_RANGE, "prefix_len[%d] = %d: needs 1 <= L and L + k + 1 <= max_len=%d", b, L, c->max_len);
+      return rv_fail(RV_E_RANGE, "prefix_len[%d] = %d: needs 1 <= L and L + k + 1 <= max_len=%d", b, L, c->max_len);
   }
   uint8_t kb[RV_MAX_BATCH];
   for (int b = 0; b < c->B; ++b) kb[b] = (uint8_t)k;
@@ -1049,21 +1018,21 @@ rv_status rv_debug_fuse_accept(rv_cache* c, const float* d_logits, const int32_t
 }
 
 rv_status rv_debug_output(const rv_cache* c, int32_t which, float* d_dst, size_t dst_bytes, void* stream) {
-  if (!c || !d_dst) return fail(RV_E_ARG, "cache and destination must not be NULL");
-  if (c->last_k < 0) return fail(RV_E_STATE, "no verify has run on this cache");
-  if (which < RV_OUT_ORIG || which > RV_OUT_MARGINS) return fail(RV_E_ARG, "unknown output %d", which);
+  if (!c || !d_dst) return rv_fail(RV_E_ARG, "cache and destination must not be NULL");
+  if (c->last_k < 0) return rv_fail(RV_E_STATE, "no verify has run on this cache");
+  if (which < RV_OUT_ORIG || which > RV_OUT_PROB_FUSED) return rv_fail(RV_E_ARG, "unknown output %d", which);
   const int k1 = c->last_k + 1;
   hipStream_t st = (hipStream_t)stream;
   if (which == RV_OUT_ENTROPY || which == RV_OUT_MARGINS) {
     const size_t n = which == RV_OUT_ENTROPY ? (size_t)2 * c->last_R1 : (size_t)c->B * (k1 + 1);
-    if (dst_bytes < n * 4) return fail(RV_E_BUFFER, "destination needs %zu bytes", n * 4);
+    if (dst_bytes < n * 4) return rv_fail(RV_E_BUFFER, "destination needs %zu bytes", n * 4);
     HIP_TRY(hipMemcpyAsync(d_dst, which == RV_OUT_ENTROPY ? c->entropy : c->margins, n * 4,
                            hipMemcpyDeviceToDevice, st),
             "copy");
     return RV_OK;
   }
   const size_t V = c->m->cfg.vocab, R1 = c->last_R1, bytes = R1 * V * 4;
-  if (dst_bytes < bytes) return fail(RV_E_BUFFER, "destination needs %zu bytes", bytes);
+  if (dst_bytes < bytes) return rv_fail(RV_E_BUFFER, "destination needs %zu bytes", bytes);
   if (which == RV_OUT_ORIG || which == RV_OUT_REFL) {
     // sequence b: logit rows 2 (b + K_b) .. (o rows, then r rows), fused rows b + K_b ..
     size_t zrow = 0;
@@ -1075,6 +1044,8 @@ rv_status rv_debug_output(const rv_cache* c, int32_t which, float* d_dst, size_t
     }
   } else if (which == RV_OUT_FUSED) {
     HIP_TRY(hipMemcpyAsync(d_dst, c->z, bytes, hipMemcpyDeviceToDevice, st), "copy");
+  } else if (which == RV_OUT_PROB_FUSED) {
+    HIP_TRY(launch_exp(c->lp + 2 * R1 * V, d_dst, R1 * V, st), "probabilities");
   } else {
     const size_t f = which - RV_OUT_LOGP_ORIG;
     HIP_TRY(hipMemcpyAsync(d_dst, c->lp + f * R1 * V, bytes, hipMemcpyDeviceToDevice, st), "copy");
@@ -1084,15 +1055,15 @@ rv_status rv_debug_output(const rv_cache* c, int32_t which, float* d_dst, size_t
 
 rv_status rv_debug_export_kv(const rv_cache* c, int32_t layer, int32_t seq, int32_t pos0, int32_t npos, void* d_k,
                              void* d_v, size_t dst_bytes, void* stream) {
-  if (!c || !d_k || !d_v) return fail(RV_E_ARG, "cache and destinations must not be NULL");
+  if (!c || !d_k || !d_v) return rv_fail(RV_E_ARG, "cache and destinations must not be NULL");
   const rv_config& mc = c->m->cfg;
   if (layer < 0 || layer >= mc.n_layers || seq < 0 || seq >= c->B || pos0 < 0 || npos <= 0 ||
       (long long)pos0 + npos > c->max_len)
-    return fail(RV_E_ARG, "layer/seq/position range outside the cache");
+    return rv_fail(RV_E_ARG, "layer/seq/position range outside the cache");
   const size_t es = c->m->es, hd = mc.head_dim, row = (size_t)npos * hd * es;
   const int planes = es == 2 ? 2 : 1;
   const size_t plane = row * mc.n_kv_heads;
-  if (dst_bytes < plane * planes) return fail(RV_E_BUFFER, "destination needs %zu bytes", plane * planes);
+  if (dst_bytes < plane * planes) return rv_fail(RV_E_BUFFER, "destination needs %zu bytes", plane * planes);
   const size_t blk = (size_t)layer * c->kv_layer_elems + (size_t)seq * mc.n_kv_heads * c->kv_len * hd;
   hipStream_t st = (hipStream_t)stream;
   if (es == 2) {
@@ -1113,9 +1084,9 @@ rv_status rv_debug_export_kv(const rv_cache* c, int32_t layer, int32_t seq, int3
 }
 
 rv_status rv_commit_tokens(rv_cache* c, const int32_t* h_pos, const int32_t* d_ids, void* stream) {
-  if (!c || !h_pos || !d_ids) return fail(RV_E_ARG, "cache, positions and ids must not be NULL");
+  if (!c || !h_pos || !d_ids) return rv_fail(RV_E_ARG, "cache, positions and ids must not be NULL");
   for (int b = 0; b < c->B; ++b)
-    if (h_pos[b] >= c->max_len) return fail(RV_E_RANGE, "position %d of sequence %d >= max_len", h_pos[b], b);
+    if (h_pos[b] >= c->max_len) return rv_fail(RV_E_RANGE, "position %d of sequence %d >= max_len", h_pos[b], b);
   for (int b = 0; b < c->B; ++b) {
     if (h_pos[b] < 0) continue;
     HIP_TRY(hipMemcpyAsync(c->ids + (size_t)b * c->max_len + h_pos[b], d_ids + b, 4, hipMemcpyDeviceToDevice,
@@ -1126,9 +1097,9 @@ rv_status rv_commit_tokens(rv_cache* c, const int32_t* h_pos, const int32_t* d_i
 }
 
 rv_status rv_debug_export_ids(const rv_cache* c, int32_t seq, int32_t pos0, int32_t n, int32_t* d_dst, void* stream) {
-  if (!c || !d_dst) return fail(RV_E_ARG, "cache and destination must not be NULL");
+  if (!c || !d_dst) return rv_fail(RV_E_ARG, "cache and destination must not be NULL");
   if (seq < 0 || seq >= c->B || pos0 < 0 || n <= 0 || (long long)pos0 + n > c->max_len)
-    return fail(RV_E_ARG, "id range outside the cache");
+    return rv_fail(RV_E_ARG, "id range outside the cache");
   HIP_TRY(hipMemcpyAsync(d_dst, c->ids + (size_t)seq * c->max_len + pos0, (size_t)n * 4, hipMemcpyDeviceToDevice,
                          (hipStream_t)stream),
           "copy");
@@ -1136,10 +1107,10 @@ rv_status rv_debug_export_ids(const rv_cache* c, int32_t seq, int32_t pos0, int3
 }
 
 rv_status rv_debug_weight_bits(const rv_model* m, int32_t tensor, const int64_t* h_idx, int32_t n, uint32_t* h_bits) {
-  if (!m || !h_idx || !h_bits || n < 0) return fail(RV_E_ARG, "bad arguments");
+  if (!m || !h_idx || !h_bits || n < 0) return rv_fail(RV_E_ARG, "bad arguments");
   const rv_config& c = m->cfg;
   const int L = c.n_layers;
-  if (tensor < 0 || tensor > 1 + 7 * L) return fail(RV_E_ARG, "tensor %d out of range", tensor);
+  if (tensor < 0 || tensor > 1 + 7 * L) return rv_fail(RV_E_ARG, "tensor %d out of range", tensor);
   const MatDesc* md = nullptr;
   const char* base = nullptr;
   int row_off = 0;
@@ -1164,7 +1135,7 @@ rv_status rv_debug_weight_bits(const rv_model* m, int32_t tensor, const int64_t*
   }
   for (int i = 0; i < n; ++i) {
     const long long idx = h_idx[i];
-    if (idx < 0 || idx >= rows * in_dim) return fail(RV_E_ARG, "index %lld out of range", idx);
+    if (idx < 0 || idx >= rows * in_dim) return rv_fail(RV_E_ARG, "index %lld out of range", idx);
     const int r = (int)(idx / in_dim), col = (int)(idx % in_dim);
     size_t off;
     if (!md) off = (size_t)idx * m->es;
@@ -1178,8 +1149,8 @@ rv_status rv_debug_weight_bits(const rv_model* m, int32_t tensor, const int64_t*
 
 rv_status rv_debug_workspace(const rv_cache* c, int32_t which, int32_t rows, void* d_dst, size_t dst_bytes,
                              void* stream) {
-  if (!c || !d_dst) return fail(RV_E_ARG, "cache and destination must not be NULL");
-  if (rows <= 0 || rows > c->rows_cap) return fail(RV_E_ARG, "rows must be in [1, %d]", c->rows_cap);
+  if (!c || !d_dst) return rv_fail(RV_E_ARG, "cache and destination must not be NULL");
+  if (rows <= 0 || rows > c->rows_cap) return rv_fail(RV_E_ARG, "rows must be in [1, %d]", c->rows_cap);
   const rv_config& mc = c->m->cfg;
   const void *src, *src2 = nullptr;
   size_t width;
@@ -1189,11 +1160,11 @@ rv_status rv_debug_workspace(const rv_cache* c, int32_t which, int32_t rows, voi
     case RV_WS_ATTN: src = c->att; src2 = c->att2; width = (size_t)mc.n_heads * mc.head_dim * es; break;
     case RV_WS_ACT: src = c->act; src2 = c->act2; width = (size_t)mc.ffn_dim * es; break;
     case RV_WS_QUERY: src = c->qbuf; src2 = c->qbuf2; width = (size_t)mc.n_heads * mc.head_dim * es; break;
-    default: return fail(RV_E_ARG, "unknown workspace buffer %d", which);
+    default: return rv_fail(RV_E_ARG, "unknown workspace buffer %d", which);
   }
   const int planes = (src2 && es == 2) ? 2 : 1;
   if (dst_bytes < width * rows * planes)
-    return fail(RV_E_BUFFER, "destination needs %zu bytes", width * rows * planes);
+    return rv_fail(RV_E_BUFFER, "destination needs %zu bytes", width * rows * planes);
   hipStream_t st = (hipStream_t)stream;
   if (!src2) {
     HIP_TRY(hipMemcpyAsync(d_dst, src, width * rows, hipMemcpyDeviceToDevice, st), "copy");
@@ -1207,15 +1178,15 @@ rv_status rv_debug_workspace(const rv_cache* c, int32_t which, int32_t rows, voi
 }
 
 rv_status rv_debug_profile(rv_cache* c, int32_t enable) {
-  if (!c) return fail(RV_E_ARG, "cache must not be NULL");
+  if (!c) return rv_fail(RV_E_ARG, "cache must not be NULL");
   c->prof = enable != 0;
   if (c->prof) c->prof_used = 0;
   return RV_OK;
 }
 
 rv_status rv_debug_profile_read(const rv_cache* c, int32_t kclass, double* total_ms, int32_t* launches) {
-  if (!c || !total_ms || !launches) return fail(RV_E_ARG, "arguments must not be NULL");
-  if (kclass < 0 || kclass >= RV_PROF_NCLASS) return fail(RV_E_ARG, "unknown kernel class %d", kclass);
+  if (!c || !total_ms || !launches) return rv_fail(RV_E_ARG, "arguments must not be NULL");
+  if (kclass < 0 || kclass >= RV_PROF_NCLASS) return rv_fail(RV_E_ARG, "unknown kernel class %d", kclass);
   double tot = 0.0;
   int n = 0;
   for (size_t i = 0; i < c->prof_used; ++i) {
@@ -1231,10 +1202,10 @@ rv_status rv_debug_profile_read(const rv_cache* c, int32_t kclass, double* total
 }
 
 rv_status rv_debug_time_matrix(rv_cache* c, int32_t matrix, int32_t M, int32_t reps, void* stream, float* avg_ms) {
-  if (!c || !avg_ms) return fail(RV_E_ARG, "cache and avg_ms must not be NULL");
-  if (M <= 0 || M > c->rows_cap || reps <= 0) return fail(RV_E_ARG, "M must be in [1, %d], reps > 0", c->rows_cap);
+  if (!c || !avg_ms) return rv_fail(RV_E_ARG, "cache and avg_ms must not be NULL");
+  if (M <= 0 || M > c->rows_cap || reps <= 0) return rv_fail(RV_E_ARG, "M must be in [1, %d], reps > 0", c->rows_cap);
   if (matrix != RV_MAT_O && matrix != RV_MAT_GATEUP && matrix != RV_MAT_DOWN && matrix != RV_MAT_LM_HEAD)
-    return fail(RV_E_ARG, "matrix %d cannot be timed", matrix);
+    return rv_fail(RV_E_ARG, "matrix %d cannot be timed", matrix);
   rv_model* m = c->m;
   const rv_config& mc = m->cfg;
   const int dt = mc.dtype, d = mc.d_model;
@@ -1265,7 +1236,7 @@ rv_status rv_debug_time_matrix(rv_cache* c, int32_t matrix, int32_t M, int32_t r
         return run_gemm(c, EPI_STORE, g, false, st);
     }
   };
-  if (matrix == RV_MAT_LM_HEAD && M > c->out_rows_cap) return fail(RV_E_ARG, "M exceeds the LM-head rows");
+  if (matrix == RV_MAT_LM_HEAD && M > c->out_rows_cap) return rv_fail(RV_E_ARG, "M exceeds the LM-head rows");
   HIP_TRY(launch(0), "warm-up launch");
   HIP_TRY(hipEventRecord(e0, st), "event");
   for (int r = 0; r < reps; ++r) HIP_TRY(launch(r), "timed launch");
@@ -1282,11 +1253,11 @@ rv_status rv_debug_time_matrix(rv_cache* c, int32_t matrix, int32_t M, int32_t r
 
 rv_status rv_debug_linear(const rv_cache* c, int32_t layer, int32_t matrix, const void* d_x, int32_t M, float* d_y,
                           size_t y_bytes, void* stream) {
-  if (!c || !d_x || !d_y) return fail(RV_E_ARG, "cache, x and y must not be NULL");
+  if (!c || !d_x || !d_y) return rv_fail(RV_E_ARG, "cache, x and y must not be NULL");
   const rv_model* m = c->m;
   const rv_config& mc = m->cfg;
-  if (matrix != RV_MAT_LM_HEAD && (layer < 0 || layer >= mc.n_layers)) return fail(RV_E_ARG, "layer out of range");
-  if (M <= 0 || M > c->rows_cap) return fail(RV_E_ARG, "M must be in [1, %d]", c->rows_cap);
+  if (matrix != RV_MAT_LM_HEAD && (layer < 0 || layer >= mc.n_layers)) return rv_fail(RV_E_ARG, "layer out of range");
+  if (M <= 0 || M > c->rows_cap) return rv_fail(RV_E_ARG, "M must be in [1, %d]", c->rows_cap);
   const MatDesc* md;
   const void* W;
   void *xbuf, *xbuf2;
@@ -1296,9 +1267,9 @@ rv_status rv_debug_linear(const rv_cache* c, int32_t layer, int32_t matrix, cons
     case RV_MAT_GATEUP: md = &m->gateup; W = m->w_gateup[layer]; xbuf = c->xn; xbuf2 = c->xn2; break;
     case RV_MAT_DOWN: md = &m->down; W = m->w_down[layer]; xbuf = c->act; xbuf2 = c->act2; break;
     case RV_MAT_LM_HEAD: md = &m->lm; W = m->lm_head; xbuf = c->xn; xbuf2 = c->xn2; break;
-    default: return fail(RV_E_ARG, "unknown matrix %d", matrix);
+    default: return rv_fail(RV_E_ARG, "unknown matrix %d", matrix);
   }
-  if (y_bytes < (size_t)M * md->N * 4) return fail(RV_E_BUFFER, "y needs %zu bytes", (size_t)M * md->N * 4);
+  if (y_bytes < (size_t)M * md->N * 4) return rv_fail(RV_E_BUFFER, "y needs %zu bytes", (size_t)M * md->N * 4);
   hipStream_t st = (hipStream_t)stream;
   const size_t plane = (size_t)M * md->K * m->es;
   HIP_TRY(launch_retile(mc.dtype, d_x, xbuf, M, md->K, true, st), "tile");

@@ -2,6 +2,7 @@
 // the kernel translation units.
 #pragma once
 #include "rv_common.h"
+#include "rv_plan.h"
 
 // ---------------------------------------------------------------- init
 hipError_t launch_init_packed(int dtype, void* dst, const MatDesc& md, uint64_t t0, uint64_t t1, uint64_t t2,
@@ -157,7 +158,6 @@ struct PlanVerify {
 };
 hipError_t launch_plan_verify(int dtype, const PlanVerify& p, hipStream_t st);
 
-enum { RV_MAX_SEGS = 128 };
 struct PlanPrefill {
   int nseg, rows, d, V, ld;
   const int* prefix;     // [B][ld]
@@ -211,3 +211,11 @@ struct HeadArgs {
   uint8_t kb[RV_MAX_BATCH];
 };
 hipError_t launch_head(const HeadArgs& a, hipStream_t st);
+// dst[i] = exp(src[i]) for i < n.
+hipError_t launch_exp(const float* src, float* dst, size_t n, hipStream_t st);
+
+// ---------------------------------------------------------------- host helpers
+// Records the calling thread's error message (rv_last_error) and returns s.
+rv_status rv_fail(rv_status s, const char* fmt, ...);
+// Validation of the fusion parameters shared by the verify entry points.
+rv_status rv_check_fusion(const rv_fusion* fusion);

@@ -46,6 +46,7 @@ class SpeculativeLoop:
         B, V = target.batch, target.shape.vocab
         self.d_drafts = torch.zeros((B, max(k, 1)), dtype=torch.int32, device="cuda")
         self.d_q = torch.zeros((B, max(k, 1), V), dtype=torch.float32, device="cuda") if rule == "sampling" else None
+        self.d_p = torch.empty((B, V), dtype=torch.float32, device="cuda") if rule == "sampling" else None
         self.rounds = 0
         self.accepted: List[int] = []
 
@@ -67,9 +68,9 @@ class SpeculativeLoop:
             if self.rule == "sampling":
                 rv.rv_verify_sampled(dr.cache, lens_d, None, 0, None, None, 0, 0.0, 0, self._round_seed(j),
                                      dr.accept_len, dr.next_id, temperature=self.T)
-                lp = torch.empty((dr.batch, 1, dr.shape.vocab), dtype=torch.float32, device="cuda")
-                rv.rv_debug_output(dr.cache, rv.RV_OUT_LOGP_FUSED, lp)
-                self.d_q[:, j].copy_(lp[:, 0].exp())
+                # the draft's distribution of its proposal, p = softmax(z), as the library emits it
+                rv.rv_debug_output(dr.cache, rv.RV_OUT_PROB_FUSED, self.d_p)
+                self.d_q[:, j].copy_(self.d_p)
             else:
                 rv.rv_verify(dr.cache, lens_d, None, 0, None, 0, 0.0, 0, dr.accept_len, dr.next_id,
                              temperature=self.T)

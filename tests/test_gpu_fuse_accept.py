@@ -61,7 +61,7 @@ def run(rv, v, o, r, drafts, alpha, L, **kw):
     rv.rv_debug_fuse_accept(v.cache, logits, L, d, k1 - 1, alpha, v.accept_len, v.next_id, **kw)
     torch.cuda.synchronize()
     v.k, v.kb = k1 - 1, None
-    out = {w: v.output(w).cpu().numpy() for w in range(8)}
+    out = {w: v.output(w).cpu().numpy() for w in range(9)}
     return v.accept_len.cpu().numpy().copy(), v.next_id.cpu().numpy().copy(), out
 
 
@@ -152,6 +152,10 @@ def test_random_rows_match_the_oracle(rv, wide, alpha):
         assert (int(n[b]), int(t[b])) == (n_ref, t_ref), b
         lp = oracle.log_softmax(z[b])
         assert np.abs(out[rv.RV_OUT_LOGP_FUSED][b] - lp).max() < 2e-5
+        # the fused distribution itself: exp of the log-probabilities, rows sum to 1
+        p = out[rv.RV_OUT_PROB_FUSED][b].astype(np.float64)
+        np.testing.assert_allclose(p, np.exp(lp), rtol=5e-5, atol=1e-12)
+        assert np.abs(p.sum(-1) - 1).max() < 1e-5
         assert np.abs(out[rv.RV_OUT_ENTROPY][0][b] - oracle.entropy(z[b])).max() < 2e-4
         assert np.abs(out[rv.RV_OUT_ENTROPY][1][b] - oracle.entropy(o[b])).max() < 2e-4
     assert int(n[1]) == k and int(n[2]) >= 2

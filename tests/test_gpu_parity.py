@@ -70,6 +70,11 @@ class Case:
             logits_close(self.shape, self.out[rv.RV_OUT_ORIG][b], ref["o"])
             logits_close(self.shape, self.out[rv.RV_OUT_REFL][b], ref["r"])
             logits_close(self.shape, self.out[rv.RV_OUT_FUSED][b], ref["z"])
+            if len(self.probe) == 0 and self.P == 0:
+                # block row k feeds both o_{k+1} and r_1 (shift = k): the LM head
+                # reads one source row twice, so the two rows agree bit for bit
+                k = self.drafts.shape[1]
+                np.testing.assert_array_equal(self.out[rv.RV_OUT_ORIG][b][k], self.out[rv.RV_OUT_REFL][b][0])
             for w in (rv.RV_OUT_LOGP_ORIG, rv.RV_OUT_LOGP_REFL, rv.RV_OUT_LOGP_FUSED):
                 s = np.exp(self.out[w][b].astype(np.float64)).sum(-1)
                 assert np.abs(s - 1).max() < 1e-4
@@ -307,6 +312,16 @@ def test_validation_errors_enqueue_nothing(rv, gpu):
     lens = v.prefill([list(range(10))])
     d = torch.zeros((1, 2), dtype=torch.int32, device="cuda")
     probe = torch.zeros(3, dtype=torch.int32, device="cuda")
+    v.accept_len.fill_(-11)
+    v.next_id.fill_(-12)
+
+    def history():
+        ids = torch.empty(40, dtype=torch.int32, device="cuda")
+        rv.rv_debug_export_ids(v.cache, 0, 0, 40, ids)
+        torch.cuda.synchronize()
+        return ids.cpu().tolist()
+
+    hist0 = history()
 
     def code(**kw):
         args = dict(prefix_len=lens, draft_ids=d, k=2, probe_ids=probe, n_probe=3, alpha=0.3, prefix_pos=2,
@@ -351,8 +366,13 @@ def test_validation_errors_enqueue_nothing(rv, gpu):
     assert code(prefix_len=[35]) == "RV_E_CAPACITY"
     assert code(n_probe=12) == "RV_E_CAPACITY"
     assert code(probe_ids=None) == "RV_E_ARG"
+    # none of the rejected calls enqueued anything: outputs and history as set above
+    torch.cuda.synchronize()
+    assert v.accept_len.cpu().tolist() == [-11] and v.next_id.cpu().tolist() == [-12]
+    assert history() == hist0
     assert code() == "RV_OK"
     torch.cuda.synchronize()
+    assert int(v.accept_len[0]) >= 0 and history() != hist0
     v.close()
 
 
