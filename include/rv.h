@@ -210,6 +210,27 @@ rv_status rv_verify_sampled(rv_cache* c, const int32_t* h_prefix_len, const int3
                             const rv_fusion* fusion, uint64_t seed, int32_t* d_accept_len,
                             int32_t* d_next_id, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * decision of rv_debug_fuse_accept -- accept_len and next_id, the same
+ * kernels and bits -- without a cache.  No id history is written and no
+ * per-row outputs are kept.  Its scratch (per-chunk softmax statistics,
+ * merged row statistics, margins) is a static device array of
+ * RV_NOALLOC_SCRATCH_BYTES that each GPU the library runs on holds until the
+ * process ends; the call allocates nothing.
+ *   d_logits [batch][2(k+1)][vocab] device fp32, as rv_debug_fuse_accept.
+ *   batch in [1, RV_MAX_BATCH], k in [0, RV_MAX_DRAFTS], vocab in [1, 262144],
+ *   and batch * (k+1) * ceil(vocab / 2048) <= 65536 (else RV_E_CAPACITY).
+ *   d_draft_ids [batch][k] device int32 (NULL if k == 0).
+ *   fusion: rule RV_RULE_GREEDY or RV_RULE_TYPICAL.
+ * Every call on one GPU uses that GPU's one array: calls that overlap on a
+ * GPU (other streams, other host threads) race and must be serialised by the
+ * caller.  Asynchronous on stream. */
+#define RV_NOALLOC_SCRATCH_BYTES (4718592)
+rv_status rv_fuse_accept_noalloc(const float* d_logits, int32_t batch, int32_t k, int32_t vocab,
+                                 const int32_t* d_draft_ids, const rv_fusion* fusion, int32_t* d_accept_len,
+                                 int32_t* d_next_id, void* stream);
+
 /* ---- inspection (tests and benchmarks) ---- */
 
 /* The fusion, log-softmax and accept stage of rv_verify (Eq. 2; Algorithm 2,

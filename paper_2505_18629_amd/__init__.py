@@ -42,7 +42,7 @@ STATUS = {0: "RV_OK", -1: "RV_E_ARG", -2: "RV_E_RANGE", -3: "RV_E_CAPACITY", -4:
 EXPORTED = [
     "rv_status_str", "rv_last_error", "rv_model_bytes", "rv_init_weights", "rv_model_free",
     "rv_cache_bytes", "rv_cache_create", "rv_cache_free", "rv_prefill_cache", "rv_verify", "rv_verify_sampled",
-    "rv_verify_ragged", "rv_commit_tokens",
+    "rv_verify_ragged", "rv_commit_tokens", "rv_fuse_accept_noalloc",
     "rv_debug_fuse_accept", "rv_debug_output", "rv_debug_export_kv", "rv_debug_export_ids", "rv_debug_weight_bits",
     "rv_debug_linear", "rv_debug_workspace", "rv_debug_profile", "rv_debug_profile_read", "rv_debug_time_matrix",
 ]
@@ -86,6 +86,7 @@ _sig = {
     "rv_commit_tokens": ([_vp, _P_i32, _vp, _vp], ctypes.c_int),
     "rv_verify_ragged": ([_vp, _P_i32, _vp, _i32, _P_i32, _vp, _i32, ctypes.POINTER(rv_fusion), _vp, _vp, _vp],
                          ctypes.c_int),
+    "rv_fuse_accept_noalloc": ([_vp, _i32, _i32, _i32, _vp, ctypes.POINTER(rv_fusion), _vp, _vp, _vp], ctypes.c_int),
     "rv_debug_fuse_accept": ([_vp, _vp, _P_i32, _vp, _i32, ctypes.POINTER(rv_fusion), _vp, _vp, _vp], ctypes.c_int),
     "rv_debug_output": ([_vp, _i32, _vp, _sz, _vp], ctypes.c_int),
     "rv_debug_export_kv": ([_vp, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp], ctypes.c_int),
@@ -219,6 +220,19 @@ def rv_verify_ragged(cache: int, prefix_len: Sequence[int], draft_ids, ld_drafts
 def rv_commit_tokens(cache: int, positions: Sequence[int], ids, stream=None) -> None:
     _keep, pos = _host_i32(positions)
     _check(_lib.rv_commit_tokens(cache, pos, _dev(ids), _stream(stream)))
+
+
+RV_NOALLOC_SCRATCH_BYTES = 4718592
+
+
+def rv_fuse_accept_noalloc(logits, k: int, draft_ids, alpha: float, accept_len, next_id,
+                           rule: int = RV_RULE_GREEDY, epsilon: float = 0.09, delta: float = 0.3,
+                           entropy_src: int = RV_ENTROPY_FUSED, temperature: float = 1.0, stream=None) -> None:
+    """logits: device fp32 [batch][2(k+1)][vocab]; no cache, scratch in the
+    library's static device array."""
+    fu = rv_fusion(alpha, 0, rule, epsilon, delta, entropy_src, temperature)
+    _check(_lib.rv_fuse_accept_noalloc(_dev(logits), logits.shape[0], k, logits.shape[-1], _dev(draft_ids),
+                                       ctypes.byref(fu), _dev(accept_len), _dev(next_id), _stream(stream)))
 
 
 def rv_debug_fuse_accept(cache: int, logits, prefix_len: Sequence[int], draft_ids, k: int, alpha: float,

@@ -12,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "librv.so")
 
-SOURCES = ["k_init.hip", "k_gemm.hip", "k_attn.hip", "k_misc.hip", "k_head.hip", "rv_api.cpp"]
+SOURCES = ["k_init.hip", "k_gemm.hip", "k_attn.hip", "k_misc.hip", "k_head.hip", "rv_noalloc.hip", "rv_api.cpp"]
 
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",

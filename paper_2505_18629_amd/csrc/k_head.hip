@@ -124,6 +124,19 @@ RV_DEV Stat stat_of(const float (&x)[E], int n_valid) {
   return r;
 }
 
+// Fused logit z_i[v] of fused row `row` whose o and r rows are lrow_o and
+// lrow_r: read back from the fused rows, or, where none are kept (z NULL),
+// recomputed from o and r with k_fuse_stats's own expression, which gives the
+// same bits.
+RV_DEV float fused_at(const HeadArgs& a, int row, int lrow_o, int lrow_r, int v) {
+  if (a.z) return a.z[(size_t)row * a.V + v];
+  const float zo = (1.0f - a.alpha) * a.logits[(size_t)lrow_o * a.V + v];
+  const float zr = a.alpha * a.logits[(size_t)lrow_r * a.V + v];
+  float z = zo + zr;
+  if (a.temp != 1.0f) z = z / a.temp;
+  return z;
+}
+
 // One workgroup per (vocabulary chunk of 2048, fused row); each thread owns 8
 // entries, strided by 256, and loads them all before computing.
 __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
@@ -134,7 +147,7 @@ __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
   const int k1 = a.kb[b] + 1, lrow0 = 2 * (row - i);  // first logit row of sequence b
   const float* o = a.logits + ((size_t)lrow0 + i) * a.V;
   const float* r = a.logits + ((size_t)lrow0 + k1 + i) * a.V;
-  float* z = a.z + (size_t)row * a.V;
+  float* z = a.z ? a.z + (size_t)row * a.V : nullptr;  // fused rows kept for inspection
   const float wa = a.alpha, wo = 1.0f - a.alpha;
   const int v0 = chunk * a.chunk, v1 = min(a.V, v0 + a.chunk);
   float ov[E], rv[E], zv[E];
@@ -158,7 +171,7 @@ __global__ __launch_bounds__(256) void k_fuse_stats(HeadArgs a) {
     if (tempered) zv[e] = zv[e] / a.temp;
     if (e < n_valid) {
       const int v = v0 + threadIdx.x + e * 256;
-      z[v] = zv[e];
+      if (z) z[v] = zv[e];
       if (zv[e] > t.m1) {
         t.m2 = t.m1;
         t.m1 = zv[e];
@@ -233,14 +246,14 @@ __global__ __launch_bounds__(512) void k_accept(HeadArgs a) {
   // row, so the serial tail below touches shared memory only.
   for (int i = w; i < k1; i += 8) {
     const int row = zrow0 + i;
-    const float* zi = a.z + (size_t)row * a.V;
+    const int lrow_o = 2 * zrow0 + i, lrow_r = 2 * zrow0 + k1 + i;  // its logit rows
     // draft id and its fused logit / probability, fetched beside the merge
     int xi = 0;
     float zxi = 0.f, qxi = 0.f;
     if (lane == 0 && i < kb) {
       xi = x[i];
       if (xi >= 0 && xi < a.V) {  // out-of-range ids are reported through row_bad
-        zxi = zi[xi];
+        zxi = fused_at(a, row, lrow_o, lrow_r, xi);
         if (a.rule == RV_RULE_SAMPLING) qxi = a.q[((size_t)b * a.k + i) * a.V + xi];
       }
     }
@@ -272,7 +285,7 @@ __global__ __launch_bounds__(512) void k_accept(HeadArgs a) {
       t.i1 = min(max(t.i1, 0), a.V - 1);  // every id used as an index below is in range
       xhat[i] = t.i1;
       top2[i] = t.m2;
-      zh[i] = zi[t.i1];
+      zh[i] = fused_at(a, row, lrow_o, lrow_r, t.i1);
       a.argmax[row] = t.i1;
       if (i < kb) {
         xs[i] = xi;
@@ -343,10 +356,12 @@ __global__ __launch_bounds__(512) void k_accept(HeadArgs a) {
   const int t = xhat[n];
   a.accept_len[b] = n;
   a.next_id[b] = t;
-  const int L = a.L[b];
-  int* hist = a.ids + (size_t)b * a.max_len;
-  for (int i = 0; i < n; ++i) hist[L + i] = xs[i];
-  hist[L + n] = t;
+  if (a.ids) {  // append x_1..x_n, t to the id history
+    const int L = a.L[b];
+    int* hist = a.ids + (size_t)b * a.max_len;
+    for (int i = 0; i < n; ++i) hist[L + i] = xs[i];
+    hist[L + n] = t;
+  }
   // bonus-token gap
   mg[a.k + 1] = zh[n] - top2[n];
 }
@@ -484,6 +499,6 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t st) {
     k_sample<<<dim3(a.nchunk, a.B), 256, 0, st>>>(a);
     k_sample_finish<<<a.B, 64, 0, st>>>(a);
   }
-  k_logprob<<<dim3(a.nchunk, 3 * R1), 256, 0, st>>>(a);
+  if (a.lp) k_logprob<<<dim3(a.nchunk, 3 * R1), 256, 0, st>>>(a);
   return hipGetLastError();
 }

@@ -194,14 +194,14 @@ struct HeadArgs {
   const float* q;        // sampling: draft distributions [B][k][V]
   uint64_t seed;         // sampling: Philox key word 0
   const float* logits;   // per sequence 2(k_b+1) rows: o rows then r rows
-  float* z;              // [R1][V], sequence b from row b + K_b
+  float* z;              // [R1][V], sequence b from row b + K_b; NULL: not kept (greedy/typical rules)
   float* part;           // [4][R1][nchunk][4]: (max, sum, centred sum) of o, r, z; z's top-2
   float* lse;            // [3][R1]
   float* entropy;        // [2][R1]: entropy of softmax(z), then of softmax(o)
-  float* lp;             // [3][R1][V]: log-softmax of o, r, z
+  float* lp;             // [3][R1][V]: log-softmax of o, r, z; NULL: not written
   float* margins;        // [B][k+2]: margins of tested drafts, then top1-top2 gap last
   const int* drafts;     // [B][k]
-  int* ids;              // history [B][max_len]
+  int* ids;              // history [B][max_len]; NULL: the decision is not appended
   const int* row_bad;    // [block rows], or NULL: logits given by the caller (draft ids checked instead)
   const int* seq_bad;    // [B] (with row_bad)
   int* accept_len;
