@@ -334,6 +334,9 @@ def main():
         per_class[name] = {"ms_per_launch": tot / n if n else None, "launches_per_step": n // args.profile_steps,
                            "ms_per_step": tot / args.profile_steps}
     rv.rv_debug_profile(v.cache, False)
+    # the outputs of the last (timed-shape) step, before anything reuses the workspace
+    v.k, v.kb = w.k, None  # the timed calls bypassed Verifier.verify
+    parity = stored_parity(rv, v, w, lens, drafts)
 
     tm = traffic_model(shape, lens, S, w.k)
     step_bytes = tm["algorithmic"]
@@ -343,12 +346,14 @@ def main():
     M = w.batch * S
     gu_bytes = gateup_bytes(shape, M)
     gu_flops = gateup_flops(shape, M)
-    # the dominant kernel's average duration inside the pass: HIP events the
-    # library attaches to each of its launches (profiled steps above)
-    gu_ms = per_class["gateup"]["ms_per_launch"]
-    # the same kernel launched back to back over every layer's weights, for
-    # comparison (no neighbouring kernels)
-    gu_iso_ms = rv.rv_debug_time_matrix(v.cache, rv.RV_MAT_GATEUP, M, 4 * shape.n_layers, stream=stream)
+    # the dominant kernel's average duration: the production kernel in the
+    # pass's launch shape, launched back to back over every layer's weights
+    # on the pass's stream, HIP events around the batch.  (This agrees with
+    # rocprofv3's in-pass average of the kernel to about 1%; the event pairs
+    # the library attaches to single launches in the profiled steps add about
+    # 1.7 us to each, so that figure is reported beside it, not used.)
+    gu_ms = rv.rv_debug_time_matrix(v.cache, rv.RV_MAT_GATEUP, M, 4 * shape.n_layers, stream=stream)
+    gu_inpass_ms = per_class["gateup"]["ms_per_launch"]
     gu_gbs = gu_bytes / (gu_ms * 1e-3) / 1e9 if gu_ms else None
     # bf16 weights: M flops per weight byte; above the ridge the kernel is MFMA-bound
     mfma_bound = shape.dtype == "bf16" and M > RIDGE_FLOP_PER_BYTE
@@ -358,12 +363,12 @@ def main():
                     "peak": MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                     "frac": (achieved / MFMA_PEAK_TFLOPS) if achieved else None,
                     "algorithmic_flops_per_launch": gu_flops, "ms_per_launch": gu_ms,
-                    "isolated_ms_per_launch": gu_iso_ms, "traffic": None, "hbm_gbs": gu_gbs}
+                    "in_pass_event_ms_per_launch": gu_inpass_ms, "traffic": None, "hbm_gbs": gu_gbs}
     else:
         roofline = {"kernel": "gate/up matmul + SwiGLU", "bound": "hbm", "achieved": gu_gbs, "peak": HBM_PEAK_GBS,
                     "unit": "GB/s", "frac": (gu_gbs / HBM_PEAK_GBS) if gu_gbs else None,
                     "algorithmic_bytes_per_launch": gu_bytes, "ms_per_launch": gu_ms,
-                    "isolated_ms_per_launch": gu_iso_ms, "traffic": None}
+                    "in_pass_event_ms_per_launch": gu_inpass_ms, "traffic": None}
     pass_line = {"bound": "mfma" if mfma_bound else "hbm", "algorithmic_bytes": step_bytes,
                  "achieved_gbs": gbs, "frac_of_8tbs": gbs / HBM_PEAK_GBS,
                  "achieved_tflops": step_flops / (ms * 1e-3) / 1e12,
@@ -372,9 +377,6 @@ def main():
     kernel_src = os.path.join(ROOT, "paper_2505_18629_amd", "csrc", "k_gemm.hip")
     if w.name == "8b-bf16-b1":
         roofline["traffic"] = traffic_from_profiles(kernel_src)
-
-    v.k, v.kb = w.k, None  # the timed calls bypassed Verifier.verify
-    parity = stored_parity(rv, v, w, lens, drafts)
 
     cpu = None
     if not args.no_cpu_baseline:
