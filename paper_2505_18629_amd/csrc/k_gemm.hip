@@ -228,10 +228,18 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
 // stored.  (Measured against 4 waves per workgroup, one per SIMD: 8B gate/up
 // at 496 tokens 223 -> 153 us, 70B down at 360 tokens 388 -> 262 us.)
 constexpr int kTiledWaves = 8;
+// k-steps whose operands are staged per barrier: two for 4 token tiles per
+// workgroup, one for 8 (whose doubled LDS staging then costs more than the
+// barrier it saves)
+template <int MT>
+constexpr int tiled_kpb() {
+  return MT <= 4 ? 2 : 1;
+}
 
-template <int NT, int MT, int EPI, int NW>
+template <int NT, int MT, int EPI, int NW, int KPB>
 __global__ __launch_bounds__(NW * 64) void k_gemm_tiled(GemmArgs a, int n_rk) {
   constexpr int DEPTH = 4;
+  static_assert(DEPTH % (2 * KPB) == 0, "the ring turns over whole pairs of LDS buffers");
   constexpr int XU = MT * 2 / NW;  // 16-byte operand chunks per thread per k-step
   static_assert(XU >= 1, "every thread stages operand chunks");
   const int lane = threadIdx.x & 63;
@@ -260,7 +268,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_tiled(GemmArgs a, int n_rk) {
     const int tt = min(tg * MT + m, last_tt);
     xsrc[u] = (const uint4*)(pl ? a.X2 : a.X) + ((size_t)tt * ksteps + kb) * 64 + l16;
   }
-  __shared__ u32x4 xs[2][2 * MT * 64];
+  __shared__ u32x4 xs[2][KPB][2 * MT * 64];
 
   f32x4_t acc[NT][MT];
 #pragma unroll
@@ -276,16 +284,16 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_tiled(GemmArgs a, int n_rk) {
 #pragma unroll
     for (int u = 0; u < XU; ++u) xq[slot][u] = *(const u32x4*)(xsrc[u] + (size_t)step * 64);
   };
-  auto stage = [&](int slot, int buf) {
+  auto stage = [&](int slot, int buf, int sub) {
 #pragma unroll
-    for (int u = 0; u < XU; ++u) xs[buf][threadIdx.x + u * NW * 64] = xq[slot][u];
+    for (int u = 0; u < XU; ++u) xs[buf][sub][threadIdx.x + u * NW * 64] = xq[slot][u];
   };
-  auto compute = [&](int slot, int buf) {
+  auto compute = [&](int slot, int buf, int sub) {
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const bf16x8_t xb = __builtin_bit_cast(bf16x8_t, xs[buf][(pl * MT + mt) * 64 + lane]);
+        const bf16x8_t xb = __builtin_bit_cast(bf16x8_t, xs[buf][sub][(pl * MT + mt) * 64 + lane]);
 #pragma unroll
         for (int nt = 0; nt < NT; ++nt)
           acc[nt][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wq[slot][nt]), xb,
@@ -295,17 +303,24 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_tiled(GemmArgs a, int n_rk) {
 
 #pragma unroll
   for (int d = 0; d < DEPTH; ++d) load(d, d);
-  stage(0, 0);
+#pragma unroll
+  for (int sub = 0; sub < KPB; ++sub) stage(sub, 0, sub);
   __syncthreads();
-  // k-step s: operands of step s+1 go to LDS, step s is computed, step
-  // s+DEPTH is fetched into the freed ring slot.
+  // Super-step h of a ring turn (KPB k-steps between barriers): the operands
+  // of the next KPB steps go to the other LDS buffer, these KPB steps are
+  // computed, and each freed ring slot fetches the step DEPTH ahead.
   for (int s0 = 0; s0 < ks; s0 += DEPTH) {
 #pragma unroll
-    for (int d = 0; d < DEPTH; ++d) {
-      const int s = s0 + d;
-      stage((d + 1) % DEPTH, (d + 1) & 1);
-      compute(d, d & 1);
-      load(d, s + DEPTH);
+    for (int h = 0; h < DEPTH / KPB; ++h) {
+      const int buf = h & 1;
+#pragma unroll
+      for (int sub = 0; sub < KPB; ++sub) stage(((h + 1) * KPB + sub) % DEPTH, buf ^ 1, sub);
+#pragma unroll
+      for (int sub = 0; sub < KPB; ++sub) {
+        const int d = h * KPB + sub;
+        compute(d, buf, sub);
+        load(d, s0 + d + DEPTH);
+      }
       __syncthreads();
     }
   }
@@ -390,10 +405,11 @@ hipError_t launch_tiled_one(const GemmArgs& a, hipStream_t st) {
   const dim3 block(NW * 64);
   LaunchEvents& ev = g_launch_events;
   if (ev.start) {
-    hipExtLaunchKernelGGL(k_gemm_tiled<NT, MT, EPI, NW>, dim3(items), block, 0, st, ev.start, ev.stop, 0, a, n_rk);
+    hipExtLaunchKernelGGL(k_gemm_tiled<NT, MT, EPI, NW, tiled_kpb<MT>()>, dim3(items), block, 0, st, ev.start, ev.stop, 0,
+                          a, n_rk);
     ev = LaunchEvents{};
   } else {
-    k_gemm_tiled<NT, MT, EPI, NW><<<items, block, 0, st>>>(a, n_rk);
+    k_gemm_tiled<NT, MT, EPI, NW, tiled_kpb<MT>()><<<items, block, 0, st>>>(a, n_rk);
   }
   return hipGetLastError();
 }
