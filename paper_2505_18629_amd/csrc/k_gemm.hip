@@ -229,8 +229,8 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
 // at 496 tokens 223 -> 153 us, 70B down at 360 tokens 388 -> 262 us.)
 constexpr int kTiledWaves = 8;
 // k-steps whose operands are staged per barrier: two for 4 token tiles per
-// workgroup, one for 8 (whose doubled LDS staging then costs more than the
-// barrier it saves)
+// workgroup (half the barriers; 14B batch 4: 16.77 -> 16.52 ms per pass), one
+// for 8 (8B batch 16 measured 18.39 -> 18.57 ms with two)
 template <int MT>
 constexpr int tiled_kpb() {
   return MT <= 4 ? 2 : 1;
