@@ -215,8 +215,8 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
 
 // ------------------------------------------------------------ many tokens
 // bf16 only, M > 64 rows (prefill chunks, large batches).  A workgroup owns
-// BN = NW * NT * 16 output rows x BM = MT * 16 tokens; its NW = 8 waves (two
-// per SIMD, so one wave's LDS and load waits overlap the other's MFMAs)
+// BN = NW * NT * 16 output rows x BM = MT * 16 tokens; its NW = 8 or 12 waves
+// (two or three per SIMD, so one wave's LDS and load waits overlap another's MFMAs)
 // split the rows (NT tiles each) and share the token tiles: each k-step's
 // operand tiles (MT tiles x hi/lo) are staged once per workgroup in
 // double-buffered LDS.  Weight tiles go straight to registers (each is used
@@ -227,7 +227,6 @@ __global__ __launch_bounds__(kWaves * 64) void k_gemm(GemmArgs a) {
 // clamped, so the pipeline has no branches; rows past M are computed and not
 // stored.  (Measured against 4 waves per workgroup, one per SIMD: 8B gate/up
 // at 496 tokens 223 -> 153 us, 70B down at 360 tokens 388 -> 262 us.)
-constexpr int kTiledWaves = 8;
 // k-steps whose operands are staged per barrier: two for 4 token tiles per
 // workgroup (half the barriers; 14B batch 4: 16.77 -> 16.52 ms per pass), one
 // for 8 (8B batch 16 measured 18.39 -> 18.57 ms with two)
@@ -240,8 +239,8 @@ template <int NT, int MT, int EPI, int NW, int KPB>
 __global__ __launch_bounds__(NW * 64) void k_gemm_tiled(GemmArgs a, int n_rk) {
   constexpr int DEPTH = 4;
   static_assert(DEPTH % (2 * KPB) == 0, "the ring turns over whole pairs of LDS buffers");
-  constexpr int XU = MT * 2 / NW;  // 16-byte operand chunks per thread per k-step
-  static_assert(XU >= 1, "every thread stages operand chunks");
+  constexpr int XCH = MT * 2 * 64;                     // 16-byte operand chunks per k-step
+  constexpr int XU = (XCH + NW * 64 - 1) / (NW * 64);  // per thread (the last round may be partial)
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int ksteps = a.K / 32;
@@ -263,7 +262,7 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_tiled(GemmArgs a, int n_rk) {
   const uint4* xsrc[XU];
 #pragma unroll
   for (int u = 0; u < XU; ++u) {
-    const int c = threadIdx.x + u * NW * 64;
+    const int c = min((int)threadIdx.x + u * NW * 64, XCH - 1);  // past XCH: a valid chunk, not staged
     const int pl = c / (MT * 64), m = (c / 64) % MT, l16 = c % 64;
     const int tt = min(tg * MT + m, last_tt);
     xsrc[u] = (const uint4*)(pl ? a.X2 : a.X) + ((size_t)tt * ksteps + kb) * 64 + l16;
@@ -286,7 +285,8 @@ __global__ __launch_bounds__(NW * 64) void k_gemm_tiled(GemmArgs a, int n_rk) {
   };
   auto stage = [&](int slot, int buf, int sub) {
 #pragma unroll
-    for (int u = 0; u < XU; ++u) xs[buf][sub][threadIdx.x + u * NW * 64] = xq[slot][u];
+    for (int u = 0; u < XU; ++u)
+      if (XCH % (NW * 64) == 0 || threadIdx.x + u * NW * 64 < XCH) xs[buf][sub][threadIdx.x + u * NW * 64] = xq[slot][u];
   };
   auto compute = [&](int slot, int buf, int sub) {
 #pragma unroll
@@ -397,9 +397,8 @@ hipError_t launch_dt(int epi, const GemmArgs& a, int nt, int mtt, hipStream_t st
   return hipErrorInvalidValue;
 }
 
-template <int NT, int MT, int EPI>
+template <int NT, int MT, int EPI, int NW>
 hipError_t launch_tiled_one(const GemmArgs& a, hipStream_t st) {
-  constexpr int NW = kTiledWaves;
   const int n_rk = a.N / (16 * NW * NT) * a.gk;
   const unsigned items = (unsigned)((n_rk + 7) / 8 * 8 * a.n_tg);
   const dim3 block(NW * 64);
@@ -415,28 +414,32 @@ hipError_t launch_tiled_one(const GemmArgs& a, hipStream_t st) {
 }
 
 template <int EPI>
-hipError_t launch_tiled_epi(const GemmArgs& a, int nt, int mt, hipStream_t st) {
-  if (nt == 4 && mt == 8) return launch_tiled_one<4, 8, EPI>(a, st);
-  if (nt == 4 && mt == 4) return launch_tiled_one<4, 4, EPI>(a, st);
-  if (nt == 2 && mt == 8) return launch_tiled_one<2, 8, EPI>(a, st);
-  if (nt == 2 && mt == 4) return launch_tiled_one<2, 4, EPI>(a, st);
+hipError_t launch_tiled_epi(const GemmArgs& a, int nw, int nt, int mt, hipStream_t st) {
+  if (nw == 8) {
+    if (nt == 4 && mt == 8) return launch_tiled_one<4, 8, EPI, 8>(a, st);
+    if (nt == 4 && mt == 4) return launch_tiled_one<4, 4, EPI, 8>(a, st);
+    if (nt == 2 && mt == 8) return launch_tiled_one<2, 8, EPI, 8>(a, st);
+    if (nt == 2 && mt == 4) return launch_tiled_one<2, 4, EPI, 8>(a, st);
+  } else if (nw == 12) {
+    if (nt == 2 && mt == 4) return launch_tiled_one<2, 4, EPI, 12>(a, st);
+  }
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int nt, int mt, hipStream_t st) {
+hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int nw, int nt, int mt, hipStream_t st) {
   const int ksteps = a.K / 32;
   if (a.gk < 1 || ksteps % a.gk || (ksteps / a.gk) % 4) return hipErrorInvalidValue;
-  if (a.N % (16 * kTiledWaves * nt)) return hipErrorInvalidValue;
+  if (nw < 1 || a.N % (16 * nw * nt)) return hipErrorInvalidValue;
   if (a.gk > 1 && epi != EPI_PARTIAL) return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_STORE: return launch_tiled_epi<EPI_STORE>(a, nt, mt, st);
-    case EPI_RESID: return launch_tiled_epi<EPI_RESID>(a, nt, mt, st);
-    case EPI_PARTIAL: return launch_tiled_epi<EPI_PARTIAL>(a, nt, mt, st);
-    case EPI_SWIGLU: return launch_tiled_epi<EPI_SWIGLU>(a, nt, mt, st);
-    case EPI_QKV: return launch_tiled_epi<EPI_QKV>(a, nt, mt, st);
-    case EPI_STORE_LOGICAL: return launch_tiled_epi<EPI_STORE_LOGICAL>(a, nt, mt, st);
+    case EPI_STORE: return launch_tiled_epi<EPI_STORE>(a, nw, nt, mt, st);
+    case EPI_RESID: return launch_tiled_epi<EPI_RESID>(a, nw, nt, mt, st);
+    case EPI_PARTIAL: return launch_tiled_epi<EPI_PARTIAL>(a, nw, nt, mt, st);
+    case EPI_SWIGLU: return launch_tiled_epi<EPI_SWIGLU>(a, nw, nt, mt, st);
+    case EPI_QKV: return launch_tiled_epi<EPI_QKV>(a, nw, nt, mt, st);
+    case EPI_STORE_LOGICAL: return launch_tiled_epi<EPI_STORE_LOGICAL>(a, nw, nt, mt, st);
   }
   return hipErrorInvalidValue;
 }

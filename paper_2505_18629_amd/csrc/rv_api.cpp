@@ -302,6 +302,7 @@ struct Prof {
 struct GemmPlan {
   bool tiled;  // many-token kernel (launch_gemm_tiled)
   int nt, mtt, n_tg, gk;
+  int nw;      // waves per workgroup of the many-token kernel
 };
 
 // part_rows: capacity of the partial buffer in rows (gk * M must fit).
@@ -320,26 +321,34 @@ GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K, bool allow_split, in
   if (dtype == RV_BF16 && M > kSplitRows && N % 256 == 0) {
     p.tiled = true;
     long long best_cost = -1, best_wgs = 0;
-    for (int mt : {8, 4})
-      for (int nt : {4, 2}) {
-        if (N % (128 * nt)) continue;
-        const int n_tg = (M + 16 * mt - 1) / (16 * mt);
-        for (int gk = 1; gk <= (allow_split ? kMaxSplitTiled : 1); gk *= 2) {
-          if (ksteps % gk || (ksteps / gk) % 4 || (gk > 1 && gk * M > part_rows)) continue;
-          const long long wgs = (long long)(N / (128 * nt)) * gk * n_tg;
-          const long long cost = (wgs + 255) / 256 * nt * mt * (ksteps / gk);
-          const bool better = best_cost < 0 || cost < best_cost || (cost == best_cost && wgs < best_wgs) ||
-                              (cost == best_cost && wgs == best_wgs && nt * mt > p.nt * p.mtt);
-          if (better) {
-            best_cost = cost;
-            best_wgs = wgs;
-            p.nt = nt;
-            p.mtt = mt;
-            p.n_tg = n_tg;
-            p.gk = gk;
-          }
+    // (waves, row tiles per wave, token tiles).  A workgroup's time goes as
+    // its waves per SIMD times each wave's work.  Twelve waves (three per
+    // SIMD, two row tiles each) give 3/4 of the 8-wave 4 x 4 workgroup's
+    // work, for matrices whose 8-wave split leaves CUs idle in a single round
+    // (14B gate/up at 172 tokens: 162 -> 216 workgroups).
+    const int shapes[][3] = {{8, 4, 8}, {8, 2, 8}, {8, 4, 4}, {8, 2, 4}, {12, 2, 4}};
+    for (const auto& sh : shapes) {
+      const int nw = sh[0], nt = sh[1], mt = sh[2];
+      if (N % (16 * nw * nt)) continue;
+      const int n_tg = (M + 16 * mt - 1) / (16 * mt);
+      for (int gk = 1; gk <= (allow_split ? kMaxSplitTiled : 1); gk *= 2) {
+        if (ksteps % gk || (ksteps / gk) % 4 || (gk > 1 && gk * M > part_rows)) continue;
+        const long long wgs = (long long)(N / (16 * nw * nt)) * gk * n_tg;
+        if (nw == 12 && wgs > 256) continue;
+        const long long cost = (wgs + 255) / 256 * nw * nt * mt * (ksteps / gk);
+        const bool better = best_cost < 0 || cost < best_cost || (cost == best_cost && wgs < best_wgs) ||
+                            (cost == best_cost && wgs == best_wgs && nt * mt > p.nt * p.mtt);
+        if (better) {
+          best_cost = cost;
+          best_wgs = wgs;
+          p.nw = nw;
+          p.nt = nt;
+          p.mtt = mt;
+          p.n_tg = n_tg;
+          p.gk = gk;
         }
       }
+    }
     if (best_cost >= 0) return p;
     p.tiled = false;
     p.gk = 1;
@@ -396,7 +405,7 @@ hipError_t run_gemm(const rv_cache* c, int epi, GemmArgs g, bool allow_split, hi
   g.gk = p.gk;
   if (gk_out) *gk_out = p.gk;
   const int e = (epi == EPI_RESID && p.gk > 1) ? EPI_PARTIAL : epi;
-  if (p.tiled) return launch_gemm_tiled(e, g, p.nt, p.mtt, st);
+  if (p.tiled) return launch_gemm_tiled(e, g, p.nw, p.nt, p.mtt, st);
   return launch_gemm(dtype, e, g, p.nt, p.mtt, st);
 }
 
