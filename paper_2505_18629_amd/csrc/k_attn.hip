@@ -177,8 +177,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a, int n_qg) {
         float mloc = -INFINITY;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt) mloc = fmaxf(mloc, fmaxf(fmaxf(s[t][kt][0], s[t][kt][1]), fmaxf(s[t][kt][2], s[t][kt][3])));
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 16, 64));
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+        mloc = rows4_max(mloc);
         const float m_new = fmaxf(m_run[t], mloc * sc);
         const float m_use = m_new == -INFINITY ? 0.f : m_new;
         const float rescale = __builtin_amdgcn_exp2f(m_run[t] - m_use);
@@ -190,8 +189,7 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a, int n_qg) {
             s[t][kt][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][kt][i], sc, -m_use));
             psum += s[t][kt][i];
           }
-        psum += __shfl_xor(psum, 16, 64);
-        psum += __shfl_xor(psum, 32, 64);
+        psum = rows4_sum(psum);
         l_run[t] = l_run[t] * rescale + psum;
         // rescale is exactly 1 where the maximum did not grow: the wave skips
         // the multiply when that holds for all its lanes

@@ -185,6 +185,26 @@ RV_DEV __host__ inline size_t mat_packed_offset(const MatDesc& m, int p, int k, 
 
 // ---------------------------------------------------------------- reductions
 
+// Reductions over the four lanes that share l % 16 (l, l^16, l^32, l^48) with
+// gfx950's row-swap permutes, which run on the VALU instead of the LDS
+// crossbar that a shuffle takes.  Swapping x with itself leaves, in the two
+// results, x's own row and the partner row (rows of 16 lanes for the first
+// swap, halves of the wave for the second), so each step combines a lane with
+// its partner in the same order for every lane of the pair: the results equal
+// two xor shuffles (16, then 32).
+RV_DEV float rows4_max(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(s[0]), __uint_as_float(s[1]));
+}
+RV_DEV float rows4_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  const auto s = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(s[0]) + __uint_as_float(s[1]);
+}
+
 RV_DEV float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
