@@ -40,9 +40,6 @@ rv_status hip_fail(hipError_t e, const char* what) {
 
 constexpr size_t kAlign = 256;
 constexpr int kVocabChunk = 2048;    // vocabulary chunk of the LM-head tail (8 entries per thread)
-constexpr int kMaxSplitK = 16;       // k-groups of a split matmul
-constexpr int kMaxSplitTiled = 4;    // k-groups of a split many-token matmul
-constexpr int kSplitRows = 64;       // matmuls with at most this many rows may split K
 
 size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 int round_up(int x, int a) { return (x + a - 1) / a * a; }
@@ -293,108 +290,10 @@ struct Prof {
   }
 };
 
-// Launch shape of one matmul: row tiles per workgroup (nt), token tiles
-// (mtt), token groups and k-groups.  Aims for >= 384 workgroups (1.5 per CU)
-// with as many rows per workgroup as possible, since every workgroup reads
-// its k-range of all operand tiles; K is split across workgroups only for
-// residual-stream outputs of few-row passes (the next RMSNorm adds the
-// partials).
-struct GemmPlan {
-  bool tiled;  // many-token kernel (launch_gemm_tiled)
-  int nt, mtt, n_tg, gk;
-  int nw;      // waves per workgroup of the many-token kernel
-};
-
-// part_rows: capacity of the partial buffer in rows (gk * M must fit).
+// The matmul launch shape for this model's element type and epilogue
+// (plan_matmul in rv_plan.h).
 GemmPlan plan_gemm(int dtype, int epi, int M, int N, int K, bool allow_split, int part_rows) {
-  constexpr int kTarget = 384;
-  const int ksteps = K / (dtype == RV_BF16 ? 32 : 16);
-  GemmPlan p{};
-  p.gk = 1;
-  // Many tokens (bf16): the LDS-tiled kernel (one 8-wave workgroup per CU)
-  // streams the weights about once for all token groups.  The shape is
-  // chosen to minimise (rounds of 256 workgroups) x (work per workgroup);
-  // ties go to fewer workgroups, then more rows and tokens per workgroup
-  // (measured over the 8B, 14B and 70B matrices at 172-496 tokens: within
-  // 6% of the best of every shape tried).  K is split only for outputs whose
-  // consumer adds k-group partials.
-  if (dtype == RV_BF16 && M > kSplitRows && N % 256 == 0) {
-    p.tiled = true;
-    long long best_cost = -1, best_wgs = 0;
-    // (waves, row tiles per wave, token tiles).  A workgroup's time goes as
-    // its waves per SIMD times each wave's work.  Twelve waves (three per
-    // SIMD, two row tiles each) give 3/4 of the 8-wave 4 x 4 workgroup's
-    // work, for matrices whose 8-wave split leaves CUs idle in a single round
-    // (14B gate/up at 172 tokens: 162 -> 216 workgroups).
-    const int shapes[][3] = {{8, 4, 8}, {8, 2, 8}, {8, 4, 4}, {8, 2, 4}, {12, 2, 4}};
-    for (const auto& sh : shapes) {
-      const int nw = sh[0], nt = sh[1], mt = sh[2];
-      if (N % (16 * nw * nt)) continue;
-      const int n_tg = (M + 16 * mt - 1) / (16 * mt);
-      for (int gk = 1; gk <= (allow_split ? kMaxSplitTiled : 1); gk *= 2) {
-        if (ksteps % gk || (ksteps / gk) % 4 || (gk > 1 && gk * M > part_rows)) continue;
-        const long long wgs = (long long)(N / (16 * nw * nt)) * gk * n_tg;
-        if (nw == 12 && wgs > 256) continue;
-        const long long cost = (wgs + 255) / 256 * nw * nt * mt * (ksteps / gk);
-        const bool better = best_cost < 0 || cost < best_cost || (cost == best_cost && wgs < best_wgs) ||
-                            (cost == best_cost && wgs == best_wgs && nt * mt > p.nt * p.mtt);
-        if (better) {
-          best_cost = cost;
-          best_wgs = wgs;
-          p.nw = nw;
-          p.nt = nt;
-          p.mtt = mt;
-          p.n_tg = n_tg;
-          p.gk = gk;
-        }
-      }
-    }
-    if (best_cost >= 0) return p;
-    p.tiled = false;
-    p.gk = 1;
-  }
-  p.mtt = M <= 16 ? 1 : M <= 32 ? 2 : 4;
-  p.n_tg = (M + 16 * p.mtt - 1) / (16 * p.mtt);
-  const int nt_min = epi == EPI_SWIGLU ? 2 : 1;
-  // Large bf16 matrices against two token tiles stream best with 8 row
-  // tiles per workgroup: half the operand re-reads per weight byte, and
-  // ~200 workgroups already saturate HBM (8B gate/up: 5.1 -> 6.0 TB/s).
-  const bool wide = dtype == RV_BF16 && p.mtt == 2 && (long long)N * K >= (32LL << 20) && N % 128 == 0;
-  if (allow_split && M <= kSplitRows && N % 64 == 0) {
-    // Prefer a launch of exactly one workgroup per CU (measured at the 8B
-    // shapes: down 8 tiles x 8 k-groups 22.6 -> 21.4 us, QKV 6 x 4
-    // 12.8 -> 11.1 us, O 4 x 4 8.3 -> 8.1 us).
-    const int nts[] = {8, 6, 4, 3, 2};
-    const int cand1[] = {2, 4, 7, 8, 14, 16};
-    for (int nt : nts) {
-      if ((nt == 8 && !wide) || (nt > 4 && p.mtt > 2) || N % (16 * nt)) continue;
-      for (int gk : cand1) {
-        if (ksteps % (4 * gk) || gk * M > part_rows) continue;
-        if ((long long)(N / (16 * nt)) * gk * p.n_tg == 256) {
-          p.nt = nt;
-          p.gk = gk;
-          return p;
-        }
-      }
-    }
-    p.nt = wide ? 8 : 4;
-    const int target = wide ? kTarget / 2 : kTarget;
-    const int cand[] = {1, 2, 4, 7, 8, 14, 16};
-    for (int gk : cand) {
-      if (ksteps % (4 * gk) || gk * M > part_rows) continue;
-      p.gk = gk;
-      if ((long long)(N / (16 * p.nt)) * gk * p.n_tg >= target) break;
-    }
-    return p;
-  }
-  if (wide && (long long)(N / 128) * p.n_tg >= kTarget / 2) {
-    p.nt = 8;
-    return p;
-  }
-  p.nt = 4;
-  while (p.nt > nt_min && (N % (16 * p.nt) || (long long)(N / (16 * p.nt)) * p.n_tg < kTarget)) p.nt /= 2;
-  while (N % (16 * p.nt)) p.nt /= 2;
-  return p;
+  return plan_matmul(dtype == RV_BF16, epi == EPI_SWIGLU, M, N, K, allow_split, part_rows);
 }
 
 hipError_t run_gemm(const rv_cache* c, int epi, GemmArgs g, bool allow_split, hipStream_t st,

@@ -1,8 +1,9 @@
 // CPU check of the library's host-side planning (rv_plan.h) at the shapes of
 // the benchmark workloads and at edge cases: every prefill chunk stays inside
 // the workspace and segment arrays and covers each sequence's positions once,
-// and every attention launch's key split fits the partial buffer and the
-// grid limits.  Built with the address and undefined-behaviour sanitizers by
+// every attention launch's key split fits the partial buffer and the grid
+// limits, and every matmul launch shape is one the launchers instantiate.
+// Built with the address and undefined-behaviour sanitizers by
 // tests/test_host_checks.py; exits non-zero on the first violation.
 #include <cstdio>
 #include <cstdlib>
@@ -102,6 +103,62 @@ void check_verify(const Shape& sh, const std::vector<int>& L, int S, int max_blo
   std::printf("%s verify B=%d S=%d: ok\n", sh.name, B, S);
 }
 
+// One matmul launch as planned: the shape must be one the launchers
+// instantiate, divide N into whole row groups and K into whole k-step
+// batches, fit the partial buffer and the grid limit.
+void check_matmul(const char* what, bool bf16, bool swiglu, bool allow_split, int M, int N, int K, int part_rows) {
+  const GemmPlan p = plan_matmul(bf16, swiglu, M, N, K, allow_split, part_rows);
+  const int ksteps = K / (bf16 ? 32 : 16);
+  CHECK(p.gk >= 1 && (p.gk == 1 || allow_split), "%s M=%d: k-groups %d", what, M, p.gk);
+  CHECK(p.gk == 1 || (long long)p.gk * M <= part_rows, "%s M=%d: %d k-groups x %d rows past %d", what, M, p.gk, M,
+        part_rows);
+  if (p.tiled) {
+    const bool known = (p.nw == 8 && (p.nt == 4 || p.nt == 2) && (p.mtt == 8 || p.mtt == 4)) ||
+                       (p.nw == 12 && p.nt == 2 && p.mtt == 4);
+    CHECK(bf16 && known, "%s M=%d: no many-token kernel (%d waves, %d x %d)", what, M, p.nw, p.nt, p.mtt);
+    CHECK(N % (16 * p.nw * p.nt) == 0, "%s M=%d: N %d not whole row groups", what, M, N);
+    CHECK(ksteps % p.gk == 0 && (ksteps / p.gk) % 4 == 0, "%s M=%d: k-steps %d / %d", what, M, ksteps, p.gk);
+    CHECK(p.n_tg * p.mtt * 16 >= M, "%s M=%d: token groups", what, M);
+    const long long rk = (long long)(N / (16 * p.nw * p.nt)) * p.gk;
+    CHECK((rk + 7) / 8 * 8 * p.n_tg < (1LL << 31), "%s M=%d: grid", what, M);
+  } else {
+    const bool nt_ok = p.nt == 1 || p.nt == 2 || p.nt == 4 || p.nt == 8 || ((p.nt == 3 || p.nt == 6) && p.gk > 1);
+    CHECK(nt_ok && (!swiglu || (p.nt % 2 == 0)), "%s M=%d: %d row tiles", what, M, p.nt);
+    CHECK((p.mtt == 1 || p.mtt == 2 || (p.mtt == 4 && p.nt <= 4)), "%s M=%d: %d token tiles with %d row tiles", what,
+          M, p.mtt, p.nt);
+    CHECK(N % (16 * p.nt) == 0, "%s M=%d: N %d, %d row tiles", what, M, N, p.nt);
+    CHECK(ksteps % (4 * p.gk) == 0, "%s M=%d: k-steps %d, %d k-groups", what, M, ksteps, p.gk);
+    CHECK(p.n_tg * p.mtt * 16 >= M, "%s M=%d: token groups", what, M);
+    CHECK((long long)p.n_tg * p.gk * (N / (16 * p.nt)) < (1LL << 31), "%s M=%d: grid", what, M);
+  }
+}
+
+// Every matmul of a pass over M rows (the verify block or a prefill chunk),
+// and the LM head over n_out rows.
+void check_matmuls(const char* name, bool bf16, int d, int hq, int hkv, int hd, int F, int V, int M, int n_out,
+                   int part_rows) {
+  const int n0 = failures;
+  const int nqkv = (hq + 2 * hkv) * hd;
+  const GemmPlan q = plan_matmul(bf16, false, M, nqkv, d, true, part_rows);
+  check_matmul("qkv", bf16, false, q.gk > 1, M, nqkv, d, part_rows);
+  check_matmul("o", bf16, false, true, M, d, hq * hd, part_rows);
+  check_matmul("gate/up", bf16, true, false, M, 2 * F, d, part_rows);
+  check_matmul("down", bf16, false, true, M, d, F, part_rows);
+  check_matmul("down (last, unsplit)", bf16, false, false, M, d, F, part_rows);
+  if (n_out > 0) check_matmul("lm head", bf16, false, false, n_out, V, d, part_rows);
+  if (failures == n0) std::printf("%s matmuls M=%d: ok\n", name, M);
+}
+
+// The matmuls of a model's verify passes and prefill chunks at several row
+// counts (full and ragged chunks, the verify block of each batch).
+void check_model_matmuls(const char* name, bool bf16, int d, int hq, int hkv, int hd, int F, int V,
+                         std::vector<int> verify_rows, int batch, int max_block) {
+  const int part_rows = std::max(kMaxSplitK * kSplitRows, kMaxSplitTiled * plan_round_up(batch * max_block, 64));
+  for (int M : verify_rows) check_matmuls(name, bf16, d, hq, hkv, hd, F, V, M, 2 * 6 * batch, part_rows);
+  for (int M : {kPrefillRows, 2047, 1023, 129, 65, 64, 33, 17, 16, 1})
+    check_matmuls(name, bf16, d, hq, hkv, hd, F, V, M, 0, part_rows);
+}
+
 }  // namespace
 
 int main() {
@@ -130,6 +187,14 @@ int main() {
   check_verify(s8, std::vector<int>(256, 300), 8, 8);
   check_prefill(s70, {2, 8192, 1, 4097}, 128, 8400);
   check_verify(s70, {2, 8192, 1, 4097}, 128, 128);
+  // matmul launch shapes: the benchmark models at their verify blocks
+  // (8B batch 1 and 16, 14B batch 4, 70B batch 8) and prefill chunks, and
+  // the tiny parity shapes
+  check_model_matmuls("8b", true, 4096, 32, 8, 128, 14336, 128256, {31, 496, 8 * 256}, 256, 64);
+  check_model_matmuls("14b", true, 5120, 40, 8, 128, 13824, 152064, {172}, 4, 64);
+  check_model_matmuls("70b", true, 8192, 64, 8, 128, 28672, 128256, {248, 360}, 8, 64);
+  check_model_matmuls("tiny-f32", false, 256, 4, 4, 64, 1024, 4096, {21, 84}, 4, 64);
+  check_model_matmuls("tiny-gqa-bf16", true, 256, 8, 2, 32, 768, 4096, {21, 84, 130}, 8, 64);
   if (failures) {
     std::fprintf(stderr, "%d failure(s)\n", failures);
     return 1;
