@@ -17,7 +17,9 @@ a fixed sample of ids (the same ids for every row of the file) plus the
 draft ids; the 16 largest fused logits (and original logits, for the alpha
 = 0 decision) with their ids; the entropies; the decisions and margins.
 
-Usage: python tests/golden/make_fulldepth.py [--only-missing] [WORKLOAD ...]
+Usage: python tests/golden/make_fulldepth.py [--only-missing] [--ckpt DIR] [WORKLOAD ...]
+(--ckpt: compute each prefix in chunks kept in DIR, so that an interrupted run
+resumes; the 70B prefix takes hours on a few host cores)
 """
 from __future__ import annotations
 
@@ -67,7 +69,34 @@ def top_list(row, n=TOP):
     return [int(i) for i in idx], f9(row[idx])
 
 
-def run_case(w, case, spec, rule, cols):
+CHUNK = 1024
+
+
+def prefix_kv(shape, seed, tokens, ckpt_dir=None, tag=""):
+    """The oracle's prefix K/V.  With ckpt_dir the prefix is computed in
+    chunks of CHUNK tokens, each chunk attending the K/V of those before it
+    (oracle.forward with past: the same causal computation), and every
+    chunk's K/V is kept in ckpt_dir, so an interrupted run resumes at the
+    first chunk not on disk."""
+    if not ckpt_dir:
+        return oracle.prefix_kv(shape, seed, tokens)
+    os.makedirs(ckpt_dir, exist_ok=True)
+    past = None
+    for c0 in range(0, len(tokens), CHUNK):
+        path = os.path.join(ckpt_dir, f"{tag}_{c0}_{len(tokens)}.npz")
+        if os.path.exists(path):
+            with np.load(path) as z:
+                ks, vs = z["k"], z["v"]
+        else:
+            _, ks, vs = oracle.forward(shape, seed, tokens[c0:c0 + CHUNK], [], return_kv=True, past=past)
+            np.savez(path + ".tmp.npz", k=ks, v=vs)
+            os.replace(path + ".tmp.npz", path)
+        past = oracle.extend_kv(past, ks, vs)
+        print(f"    prefix chunk {c0}..{min(c0 + CHUNK, len(tokens)) - 1} of {len(tokens)}", flush=True)
+    return past
+
+
+def run_case(w, case, spec, rule, cols, ckpt_dir=None):
     shape = w.shape
     lens = [int(x) for x in workload.prefix_lengths(w, case)]
     prefixes = [[int(t) for t in p] for p in workload.prefix_ids(w, lens, case)]
@@ -78,7 +107,7 @@ def run_case(w, case, spec, rule, cols):
     seqs = []
     for b in check:
         t0 = time.time()
-        past = oracle.prefix_kv(shape, w.weight_seed, prefixes[b][:-1])
+        past = prefix_kv(shape, w.weight_seed, prefixes[b][:-1], ckpt_dir, f"{w.name}_c{case}_s{b}")
         t1 = time.time()
         greedy = oracle.greedy_continuation(shape, w.weight_seed, prefixes[b], w.k, past=past)
         if rule == "greedy":
@@ -115,7 +144,7 @@ def run_case(w, case, spec, rule, cols):
     return {"case": case, "drafts_rule": rule, "prefix_len": lens, "drafts": drafts, "sequences": seqs}
 
 
-def main(names, only_missing=False):
+def main(names, only_missing=False, ckpt_dir=None):
     """Writes each workload's file; with only_missing, keeps the cases an
     existing file already holds and computes the others."""
     for name in names:
@@ -138,7 +167,7 @@ def main(names, only_missing=False):
                 c["drafts_rule"] = rule
                 out["cases"].append(c)
             else:
-                out["cases"].append(run_case(w, case, spec, rule, cols))
+                out["cases"].append(run_case(w, case, spec, rule, cols, ckpt_dir))
         with open(path, "w") as f:
             json.dump(out, f, separators=(",", ":"))
         print(f"wrote {path} ({os.path.getsize(path) / 1e3:.0f} kB)", flush=True)
@@ -147,5 +176,10 @@ def main(names, only_missing=False):
 if __name__ == "__main__":
     args = sys.argv[1:]
     missing = "--only-missing" in args
+    ckpt = None
+    if "--ckpt" in args:
+        i = args.index("--ckpt")
+        ckpt = args[i + 1]
+        del args[i:i + 2]
     args = [a for a in args if a != "--only-missing"]
-    main(args or list(PLAN), missing)
+    main(args or list(PLAN), missing, ckpt)
