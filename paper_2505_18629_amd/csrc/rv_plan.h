@@ -111,7 +111,7 @@ inline GemmPlan plan_matmul(bool bf16, bool swiglu, int M, int N, int K, bool al
   const int ksteps = K / (bf16 ? 32 : 16);
   GemmPlan p{};
   p.gk = 1;
-  // Many tokens (bf16): the LDS-tiled kernel (one 8-wave workgroup per CU)
+  // Many tokens (bf16): the LDS-tiled kernel (one 8- or 12-wave workgroup per CU)
   // streams the weights about once for all token groups.  The shape is
   // chosen to minimise (rounds of 256 workgroups) x (work per workgroup);
   // ties go to fewer workgroups, then more rows and tokens per workgroup
