@@ -420,6 +420,7 @@ hipError_t launch_tiled_epi(const GemmArgs& a, int nw, int nt, int mt, hipStream
     if (nt == 4 && mt == 4) return launch_tiled_one<4, 4, EPI, 8>(a, st);
     if (nt == 2 && mt == 8) return launch_tiled_one<2, 8, EPI, 8>(a, st);
     if (nt == 2 && mt == 4) return launch_tiled_one<2, 4, EPI, 8>(a, st);
+    if (nt == 2 && mt == 6) return launch_tiled_one<2, 6, EPI, 8>(a, st);
   } else if (nw == 12) {
     if (nt == 2 && mt == 4) return launch_tiled_one<2, 4, EPI, 12>(a, st);
   }

@@ -114,7 +114,7 @@ void check_matmul(const char* what, bool bf16, bool swiglu, bool allow_split, in
         part_rows);
   if (p.tiled) {
     const bool known = (p.nw == 8 && (p.nt == 4 || p.nt == 2) && (p.mtt == 8 || p.mtt == 4)) ||
-                       (p.nw == 12 && p.nt == 2 && p.mtt == 4);
+                       (p.nw == 8 && p.nt == 2 && p.mtt == 6) || (p.nw == 12 && p.nt == 2 && p.mtt == 4);
     CHECK(bf16 && known, "%s M=%d: no many-token kernel (%d waves, %d x %d)", what, M, p.nw, p.nt, p.mtt);
     CHECK(N % (16 * p.nw * p.nt) == 0, "%s M=%d: N %d not whole row groups", what, M, N);
     CHECK(ksteps % p.gk == 0 && (ksteps / p.gk) % 4 == 0, "%s M=%d: k-steps %d / %d", what, M, ksteps, p.gk);
