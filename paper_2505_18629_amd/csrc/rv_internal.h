@@ -60,7 +60,7 @@ struct GemmArgs {
 // mtt: token tiles (1, 2, 4; 1 or 2 with nt = 8).
 hipError_t launch_gemm(int dtype, int epi, const GemmArgs& a, int nt, int mtt, hipStream_t st);
 // bf16, many tokens: nw*nt*16 rows x mt*16 tokens per workgroup of nw waves ((nw, nt, mt)
-// one of (8, 4, 8), (8, 4, 4), (8, 2, 8), (8, 2, 4), (12, 2, 4)), n_tg = ceil(M / (mt*16))
+// one of (8, 4, 8), (8, 4, 4), (8, 2, 8), (8, 2, 4), (8, 2, 6), (12, 2, 4)), n_tg = ceil(M / (mt*16))
 // token groups; N % (16*nw*nt) == 0; gk k-groups of a multiple of 4 k-steps each (gk > 1
 // only with EPI_PARTIAL).
 hipError_t launch_gemm_tiled(int epi, const GemmArgs& a, int nw, int nt, int mt, hipStream_t st);
