@@ -40,13 +40,12 @@ constexpr int kKB = 64;  // keys per LDS tile
 // -inf, so P is exactly 0) or belong to queries whose results are not stored.
 template <int HD, int NW, int TPW>
 __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a, int n_qg) {
-  static_assert(NW * TPW == 8, "a workgroup covers 128 queries");
+  constexpr int QPW = NW * TPW * 16;          // queries per workgroup
   constexpr int DC = HD / 32;                 // d chunks for QK^T
   constexpr int DT = HD / 16;                 // d tiles for PV
   constexpr int SPAN = kKB * HD;              // elements of one plane of a tile
   constexpr int UNITS = 4 * SPAN / 512;       // 1 KiB units per tile (4 spans)
-  constexpr int UPW = UNITS / NW;             // units each wave copies
-  static_assert(UNITS % NW == 0, "tile units must divide among the waves");
+  constexpr int UPW = (UNITS + NW - 1) / NW;  // units each wave copies (the last round may be partial)
   __shared__ __attribute__((aligned(16))) uint16_t sm0[4][SPAN];
   __shared__ __attribute__((aligned(16))) uint16_t sm1[4][SPAN];
 
@@ -62,9 +61,9 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a, int n_qg) {
   const int G = a.n_heads / a.n_kv;
   const int nrows = a.seg_n[seg], row0 = a.seg_row0[seg], pos0 = a.seg_pos0[seg], b = a.seg_b[seg];
   const int Q = G * nrows;
-  const int q_begin = qg * 128;
+  const int q_begin = qg * QPW;
   if (q_begin >= Q) return;
-  const int q_end = min(Q, q_begin + 128);
+  const int q_end = min(Q, q_begin + QPW);
   const int kmax = pos0 + (q_end - 1) / G + 1;
   const int kbeg = split * a.ks, kend = min(kmax, kbeg + a.ks);
   const int qpos_min = pos0 + q_begin / G;
@@ -74,21 +73,37 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a, int n_qg) {
   const int qd = a.n_heads * HD;
   const size_t kvoff = (size_t)(b * a.n_kv + kvh) * a.kv_len * HD;
 
-  // the spans this wave copies: unit u of the tile is span u / (UNITS/4)
-  const uint16_t* src[UPW];
-  int dst[UPW];
+  // The units this wave copies: with NW dividing the tile's units, a run of
+  // UPW consecutive units (addresses kept per lane); otherwise units w,
+  // w + NW, ... (addresses formed per copy).  Unit u is span u / (UNITS/4).
+  const uint16_t* src[UNITS % NW == 0 ? UPW : 1];
+  int dst[UNITS % NW == 0 ? UPW : 1];
+  if constexpr (UNITS % NW == 0) {
 #pragma unroll
-  for (int i = 0; i < UPW; ++i) {
-    const int u = w * UPW + i, sp = u / (UNITS / 4), off = (u % (UNITS / 4)) * 512;
-    const void* base = sp == 0 ? a.kc : sp == 1 ? a.kc2 : sp == 2 ? a.vc : a.vc2;
-    src[i] = (const uint16_t*)base + kvoff + off + lane * 8;
-    dst[i] = sp * SPAN + off;
+    for (int i = 0; i < UPW; ++i) {
+      const int u = w * UPW + i, sp = u / (UNITS / 4), off = (u % (UNITS / 4)) * 512;
+      const void* base = sp == 0 ? a.kc : sp == 1 ? a.kc2 : sp == 2 ? a.vc : a.vc2;
+      src[i] = (const uint16_t*)base + kvoff + off + lane * 8;
+      dst[i] = sp * SPAN + off;
+    }
   }
   auto fetch = [&](uint16_t(&sm)[4][SPAN], int kt0) {
 #pragma unroll
-    for (int i = 0; i < UPW; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(src[i] + (size_t)kt0 * HD),
-                                       (__attribute__((address_space(3))) void*)(&sm[0][0] + dst[i]), 16, 0, 0);
+    for (int i = 0; i < UPW; ++i) {
+      if constexpr (UNITS % NW == 0) {
+        __builtin_amdgcn_global_load_lds((const void*)(src[i] + (size_t)kt0 * HD),
+                                         (__attribute__((address_space(3))) void*)(&sm[0][0] + dst[i]), 16, 0, 0);
+      } else {
+        const int u = w + i * NW;
+        if (u < UNITS) {
+          const int sp = u / (UNITS / 4), off = (u % (UNITS / 4)) * 512;
+          const uint16_t* base = (const uint16_t*)(sp == 0 ? a.kc : sp == 1 ? a.kc2 : sp == 2 ? a.vc : a.vc2);
+          __builtin_amdgcn_global_load_lds((const void*)(base + kvoff + (size_t)kt0 * HD + off + lane * 8),
+                                           (__attribute__((address_space(3))) void*)(&sm[0][0] + sp * SPAN + off),
+                                           16, 0, 0);
+        }
+      }
+    }
   };
   if (kbeg < kend) fetch(sm0, kbeg);
 
@@ -123,8 +138,13 @@ __global__ __launch_bounds__(NW * 64) void k_attn_bf16(AttnArgs a, int n_qg) {
 #pragma unroll
     for (int d = 0; d < DT; ++d) O[t][d] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // Waves whose query tiles all lie past q_end (a workgroup of more queries
+  // than the segment has) copy their share of each tile and skip the rest.
+  const bool active = q_begin + TPW * w * 16 < q_end;
+
   // One 64-key tile from the LDS buffer sm.
   auto tile = [&](const uint16_t(&sm)[4][SPAN], int kt0) {
+    if (!active) return;
     // scores for 64 keys x TPW query tiles
     f32x4_t s[TPW][4];
 #pragma unroll
@@ -422,15 +442,26 @@ hipError_t launch_export_kv(const void* src_hi, const void* src_lo, int hd, int 
   return hipGetLastError();
 }
 
-hipError_t launch_attention(int dtype, const AttnArgs& a, int n_qgroups, hipStream_t st) {
+hipError_t launch_attention(int dtype, const AttnArgs& a, int n_qgroups, int qpw, hipStream_t st) {
   const int groups = a.nseg * a.n_kv;
   if (dtype == RV_BF16) {
     const unsigned units = (unsigned)(a.nsplit * groups);
     const dim3 grid((units + 7) / 8 * 8 * n_qgroups);
+    if (qpw != 128 && qpw != 192) return hipErrorInvalidValue;
+    const bool w12 = qpw == 192;
     switch (a.hd) {
-      case 32: k_attn_bf16<32, 8, 1><<<grid, 512, 0, st>>>(a, n_qgroups); break;
-      case 64: k_attn_bf16<64, 8, 1><<<grid, 512, 0, st>>>(a, n_qgroups); break;
-      case 128: k_attn_bf16<128, 8, 1><<<grid, 512, 0, st>>>(a, n_qgroups); break;
+      case 32:
+        if (w12) k_attn_bf16<32, 12, 1><<<grid, 768, 0, st>>>(a, n_qgroups);
+        else k_attn_bf16<32, 8, 1><<<grid, 512, 0, st>>>(a, n_qgroups);
+        break;
+      case 64:
+        if (w12) k_attn_bf16<64, 12, 1><<<grid, 768, 0, st>>>(a, n_qgroups);
+        else k_attn_bf16<64, 8, 1><<<grid, 512, 0, st>>>(a, n_qgroups);
+        break;
+      case 128:
+        if (w12) k_attn_bf16<128, 12, 1><<<grid, 768, 0, st>>>(a, n_qgroups);
+        else k_attn_bf16<128, 8, 1><<<grid, 512, 0, st>>>(a, n_qgroups);
+        break;
       default: return hipErrorInvalidValue;
     }
   } else {

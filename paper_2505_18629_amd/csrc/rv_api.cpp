@@ -320,10 +320,11 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, c
   const int G = mc.n_heads / mc.n_kv_heads;
   const int qmax = G * max_seg_rows;
   const int groups = nseg * mc.n_kv_heads;
-  const int qgroups = (qmax + 127) / 128;
+  const int qpw = plan_attn_queries(dt == RV_BF16, qmax);
+  const int qgroups = (qmax + qpw - 1) / qpw;
   // Key split (plan_attn_split; 70B batch 8 at 8K context: 4 splits, 768
   // workgroups, 348 us per layer vs 393 us with 3 splits and 576).
-  const int ks = plan_attn_split(kmax, nseg, h_seg_end, h_seg_rows, mc.n_kv_heads, G, qmax, c->part_entries);
+  const int ks = plan_attn_split(kmax, nseg, h_seg_end, h_seg_rows, mc.n_kv_heads, G, qmax, c->part_entries, qpw);
   if (ks == 0) return rv_fail(RV_E_CAPACITY, "attention partial buffer too small for %d keys", kmax);
   const int nsplit = (kmax + ks - 1) / ks;
 
@@ -412,7 +413,7 @@ rv_status run_layers(rv_cache* c, int M, int nseg, int max_seg_rows, int kmax, c
     at.vc2 = vc2;
     {
       Prof pf(c, RV_PROF_ATTN, st);
-      HIP_TRY(launch_attention(dt, at, qgroups, st), "attention");
+      HIP_TRY(launch_attention(dt, at, qgroups, qpw, st), "attention");
     }
     {
       Prof pf(c, RV_PROF_COMBINE, st);

@@ -91,7 +91,8 @@ struct AttnArgs {
   void* out2;           // lo plane
   float scale_log2;     // log2(e) / sqrt(hd)
 };
-hipError_t launch_attention(int dtype, const AttnArgs& a, int n_qgroups, hipStream_t st);
+// qpw: queries per workgroup (plan_attn_queries; 192 for bf16 only), n_qgroups = ceil(qmax / qpw).
+hipError_t launch_attention(int dtype, const AttnArgs& a, int n_qgroups, int qpw, hipStream_t st);
 hipError_t launch_attn_combine(int dtype, const AttnArgs& a, hipStream_t st);
 // Copies positions pos0 .. pos0+npos-1 of every kv head of one sequence out of
 // a bf16 K (is_v false) or V cache block into row-major planes

@@ -65,15 +65,21 @@ inline bool next_prefill_chunk(const int* L, int B, int rows_cap, int& b, int& p
   return true;
 }
 
+// Queries per workgroup of the bf16 attention kernel: 128 (8 waves of one
+// 16-query tile), or 192 (12 waves) when a kv head has 129-192 queries,
+// which would otherwise take a second, mostly idle group of 128 (14B verify
+// block: 155 queries; 4 x 2048 keys, 30.4-32.7 -> 27.5-29.0 us per launch).
+inline int plan_attn_queries(bool bf16, int qmax) { return bf16 && qmax > 128 && qmax <= 192 ? 192 : 128; }
+
 // Key split of one attention launch (a multiple of 64 keys), or 0 if none
 // fits.  Minimises the estimated time: rounds of 256 workgroups (one per CU)
 // x (64-key tiles per workgroup + a per-workgroup overhead of about two
 // tiles), counting the workgroups that have keys (segment s has keys
 // 0 .. seg_end[s]-1 and G * seg_rows[s] queries per kv head, in groups of
-// 128); bounded by the partial buffer (splits x segments x kv heads x qmax
+// qpw); bounded by the partial buffer (splits x segments x kv heads x qmax
 // entries) and by the combine kernel's kMaxKeySplits splits per query.
 inline int plan_attn_split(int kmax, int nseg, const int* seg_end, const int* seg_rows, int n_kv, int G, int qmax,
-                           size_t part_entries) {
+                           size_t part_entries, int qpw = 128) {
   const int groups = nseg * n_kv;
   int ks = 0;
   double best = 0;
@@ -82,7 +88,7 @@ inline int plan_attn_split(int kmax, int nseg, const int* seg_end, const int* se
     if (ns > kMaxKeySplits || (size_t)ns * groups * qmax > part_entries) continue;
     long long wgs = 0;
     for (int s = 0; s < nseg; ++s)
-      wgs += (long long)((seg_end[s] + cand - 1) / cand) * n_kv * ((G * seg_rows[s] + 127) / 128);
+      wgs += (long long)((seg_end[s] + cand - 1) / cand) * n_kv * ((G * seg_rows[s] + qpw - 1) / qpw);
     const double t = (double)((wgs + 255) / 256) * (cand / 64 + 2);
     if (ks == 0 || t < best) {
       best = t;

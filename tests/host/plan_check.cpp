@@ -37,13 +37,15 @@ void check_attention(const Shape& sh, int kmax, int nseg, const int* seg_end, co
                      size_t part_entries, const char* what) {
   const int G = sh.n_heads / sh.n_kv;
   const int qmax = G * max_seg_rows;
-  const int ks = plan_attn_split(kmax, nseg, seg_end, seg_rows, sh.n_kv, G, qmax, part_entries);
+  const int qpw = plan_attn_queries(true, qmax);
+  CHECK(qpw == 128 || qpw == 192, "%s %s: %d queries per workgroup", sh.name, what, qpw);
+  const int ks = plan_attn_split(kmax, nseg, seg_end, seg_rows, sh.n_kv, G, qmax, part_entries, qpw);
   CHECK(ks > 0 && ks % 64 == 0, "%s %s: no key split for kmax %d", sh.name, what, kmax);
   const long long nsplit = (kmax + ks - 1) / ks;
   CHECK(nsplit <= kMaxKeySplits, "%s %s: %lld splits", sh.name, what, nsplit);
   CHECK((size_t)nsplit * nseg * sh.n_kv * qmax <= part_entries, "%s %s: partial entries", sh.name, what);
   const long long units = nsplit * nseg * sh.n_kv;
-  const long long grid = (units + 7) / 8 * 8 * ((qmax + 127) / 128);
+  const long long grid = (units + 7) / 8 * 8 * ((qmax + qpw - 1) / qpw);
   CHECK(grid > 0 && grid < (1LL << 31), "%s %s: attention grid %lld", sh.name, what, grid);
   CHECK((long long)(qmax + 3) / 4 < (1LL << 31) && (long long)nseg * sh.n_kv < 65536, "%s %s: combine grid", sh.name,
         what);

@@ -144,7 +144,9 @@ def test_tiny_f32_batch_ragged(rv, gpu):
     c.v.close()
 
 
-@pytest.mark.parametrize("alpha,P,n_probe,k", [(0.3, 4, 8, 4), (1.0, 2, 3, 2), (0.0, 0, 0, 0)])
+# (0.3, 4, 16, 8): 37 block rows x 4 query heads per kv head = 148 queries,
+# the 192-query (12-wave) attention workgroup
+@pytest.mark.parametrize("alpha,P,n_probe,k", [(0.3, 4, 8, 4), (1.0, 2, 3, 2), (0.0, 0, 0, 0), (0.3, 4, 16, 8)])
 def test_tiny_bf16_gqa_matches_oracle(rv, gpu, alpha, P, n_probe, k):
     shape = workload.TINY_GQA_BF16
     hists = [workload.random_ids(shape.vocab, L, 2, b) for b, L in enumerate([40, 150, 300])]
