@@ -67,8 +67,9 @@ inline bool next_prefill_chunk(const int* L, int B, int rows_cap, int& b, int& p
 
 // Queries per workgroup of the bf16 attention kernel: 128 (8 waves of one
 // 16-query tile), or 192 (12 waves) when a kv head has 129-192 queries,
-// which would otherwise take a second, mostly idle group of 128 (14B verify
-// block: 155 queries; 4 x 2048 keys, 30.4-32.7 -> 27.5-29.0 us per launch).
+// which would otherwise take a second, mostly idle group of 128 (5 query
+// heads per kv head x 31 block rows = 155, e.g. the 14B shape at k = 5 with a
+// 16-token probe: 4 x 2048 keys, 30.4-32.7 -> 27.5-29.0 us per launch).
 inline int plan_attn_queries(bool bf16, int qmax) { return bf16 && qmax > 128 && qmax <= 192 ? 192 : 128; }
 
 // Key split of one attention launch (a multiple of 64 keys), or 0 if none
