@@ -8,9 +8,10 @@
 // argument for unidirectional attention, Section 3.1), and the probe and
 // second copy see everything before them.
 //
-// Work split: one workgroup per (key split, query group of 128, segment x kv
-// head).  The G = Hq/Hkv query heads of a kv head share each K/V tile, so a
-// verify block of S rows gives G*S queries per kv head (124 for the 8B shape).
+// Work split: one workgroup per (key split, query group of 128 -- or 192 when
+// a kv head has 129-192 queries -- segment x kv head).  The G = Hq/Hkv query
+// heads of a kv head share each K/V tile, so a verify block of S rows gives
+// G*S queries per kv head (124 for the 8B shape).
 // Each split writes unnormalised partial results; a second kernel combines
 // splits in a fixed order (deterministic).
 #include "rv_internal.h"
