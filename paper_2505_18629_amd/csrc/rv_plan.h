@@ -176,8 +176,11 @@ inline GemmPlan plan_matmul(bool bf16, bool swiglu, int M, int N, int K, bool al
   if (allow_split && M <= kSplitRows && N % 64 == 0) {
     // Prefer a launch of exactly one workgroup per CU (measured at the 8B
     // shapes: down 8 tiles x 8 k-groups 22.6 -> 21.4 us, QKV 6 x 4
-    // 12.8 -> 11.1 us, O 4 x 4 8.3 -> 8.1 us).
-    const int nts[] = {8, 6, 4, 3, 2};
+    // 12.8 -> 11.1 us, O 4 x 4 8.3 -> 8.1 us), with 4 and 3 row tiles tried
+    // before 6: the QKV then runs 3 tiles x 2 k-groups, half the partials
+    // for the finish kernel to add (the 8B batch-1 pass 3.951 -> 3.944 ms;
+    // O as 2 x 2 and down as 2 x 2 or 4 x 4 measured slower).
+    const int nts[] = {8, 4, 3, 6, 2};
     const int cand1[] = {2, 4, 7, 8, 14, 16};
     for (int nt : nts) {
       if ((nt == 8 && !wide) || (nt > 4 && p.mtt > 2) || N % (16 * nt)) continue;
