@@ -1,7 +1,8 @@
 """GPU path vs the CPU oracle on small configurations (through the C ABI).
 
 Bars: accept_len / next_id identical unless the oracle flags a near-tie
-(a decision margin within 1e-3 in fused-logit units); logits max-abs <= 1e-4
+(a decision margin within 1e-3 in fused-logit units), where they must be a
+decision the oracle's rows allow within 1e-3 (tests/decisions.py); logits max-abs <= 1e-4
 for fp32 models, per-row max|diff| / max|ref| <= 2e-2 for bf16 models;
 log-softmax rows sum to 1.
 """
@@ -10,6 +11,7 @@ import pytest
 
 import oracle
 import workload
+from decisions import greedy_allowed, typical_allowed
 
 pytestmark = pytest.mark.gpu
 
@@ -85,14 +87,19 @@ class Case:
             h_tol = 5e-4 if self.shape.dtype == "f32" else 2e-2 * max(1.0, float(np.abs(ref["h_z"]).max()))
             assert np.abs(self.out[rv.RV_OUT_ENTROPY][0][b] - ref["h_z"]).max() < h_tol
             assert np.abs(self.out[rv.RV_OUT_ENTROPY][1][b] - ref["h_o"]).max() < h_tol
+            n, t = int(self.accept_len[b]), int(self.next_id[b])
             if not ref["near_tie"]:
-                assert (int(self.accept_len[b]), int(self.next_id[b])) == (ref["accept_len"], ref["next_id"]), (
-                    b, ref["margins"], ref["gap"])
+                assert (n, t) == (ref["accept_len"], ref["next_id"]), (b, ref["margins"], ref["gap"])
                 mg = self.out[rv.RV_OUT_MARGINS][b]
                 n_tested = len(ref["margins"])
                 m_tol = 1e-3 if self.shape.dtype == "f32" else 5e-2
                 np.testing.assert_allclose(mg[:n_tested], ref["margins"], atol=m_tol)
                 assert np.isnan(mg[n_tested:-1]).all()
+            elif self.typical:
+                eps, delta, src = self.typical
+                assert typical_allowed(ref["z"], ref["o"], self.drafts[b], n, t, eps, delta, src), (b, n, t)
+            else:
+                assert greedy_allowed(ref["z"], self.drafts[b], n, t), (b, n, t, ref["margins"], ref["gap"])
         return True
 
 
@@ -413,6 +420,10 @@ def test_ragged_draft_counts_match_oracle(rv, gpu, shape, typical):
         assert np.abs(out[rv.RV_OUT_ENTROPY][0][rows] - ref["h_z"]).max() < h_tol
         if not ref["near_tie"]:
             assert (int(acc[b]), int(nxt[b])) == (ref["accept_len"], ref["next_id"]), (b, ref["margins"])
+        elif typical:
+            assert typical_allowed(ref["z"], ref["o"], drafts[b], int(acc[b]), int(nxt[b]), *typical), b
+        else:
+            assert greedy_allowed(ref["z"], drafts[b], int(acc[b]), int(nxt[b])), (b, ref["margins"])
         # history: prefix + accepted drafts + t
         n = int(acc[b])
         ids = torch.empty(lens[b] + n + 1, dtype=torch.int32, device="cuda")

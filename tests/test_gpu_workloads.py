@@ -18,6 +18,7 @@ import pytest
 
 import oracle
 import workload
+from decisions import greedy_allowed
 
 pytestmark = pytest.mark.gpu
 
@@ -85,6 +86,8 @@ def test_workload_one_layer_matches_oracle(rv, gpu, name, case):
             assert np.abs(outs["lp_z"][i] - lp_ref).max() < 2e-3, (name, b, alpha)
             if not near:
                 assert (int(acc[i]), int(nxt[i])) == (n_ref, t_ref), (name, b, alpha)
+            else:
+                assert greedy_allowed(z_ref, drafts[b], int(acc[i]), int(nxt[i])), (name, b, alpha)
             if alpha == 0.0 and not near:
                 assert int(acc[i]) >= 1, (name, b)
 
