@@ -6,8 +6,10 @@
   by one from its own weight generator).
 * A reduced-depth model with the 8B widths (2 layers, vocab 128256): full
   verify parity against the oracle.
-* The full 8B-shaped verify (32 layers, prefix 1024), where the oracle cannot
-  recompute a whole pass: properties that hold at any size.
+* The full 8B-shaped verify (32 layers, prefix 1024): properties that hold
+  at any size (Eq. 2 exactly, log-softmax sums, the rule on its own logits,
+  repeatability, probe independence).  The comparison of that whole pass with
+  the oracle is in test_gpu_fulldepth.py, against results the oracle stored.
 """
 import numpy as np
 import pytest
