@@ -410,6 +410,7 @@ def main():
         "algorithmic_flops_per_step": step_flops,
         "wall_s_timed": t_wall,
         "accept_len": accept,
+        "accept_len_hist": {str(n): accept.count(n) for n in sorted(set(accept))},
         "roofline": roofline,
         "pass": pass_line,
         "parity": parity,
