@@ -135,9 +135,12 @@ inline GemmPlan plan_matmul(bool bf16, bool swiglu, int M, int N, int K, bool al
     // (14B gate/up at 172 tokens: 162 -> 216 workgroups); six token tiles
     // do the same for widths that twelve waves do not divide (14B QKV at
     // 172 tokens: 168 -> 224 workgroups, 39.8 -> 35.3 us).  Equal costs go
-    // to fewer workgroups, then more waves per workgroup (the 14B gate/up:
-    // 12 waves x 4 tokens tiles 104 us, 8 waves x 6 token tiles 108 us),
-    // then larger tiles.
+    // to fewer workgroups, then more row tiles per wave (each staged operand
+    // tile feeds that many MFMAs, so the LDS reads per MFMA halve from 2 to
+    // 4: O and down as 4 x 4 instead of 2 x 8, 8B batch 16 17.91 -> 17.76
+    // ms, 70B 126.9 -> 124.9 ms), then more waves per workgroup (the 14B
+    // gate/up: 12 waves x 4 tokens tiles 104 us, 8 waves x 6 token tiles
+    // 108 us), then larger tiles.
     const int shapes[][3] = {{8, 4, 8}, {8, 2, 8}, {8, 4, 4}, {8, 2, 4}, {12, 2, 4}, {8, 2, 6}};
     for (const auto& sh : shapes) {
       const int nw = sh[0], nt = sh[1], mt = sh[2];
@@ -149,8 +152,9 @@ inline GemmPlan plan_matmul(bool bf16, bool swiglu, int M, int N, int K, bool al
         if (nw == 12 && wgs > 256) continue;
         const long long cost = (wgs + 255) / 256 * nw * nt * mt * (ksteps / gk);
         const bool better = best_cost < 0 || cost < best_cost || (cost == best_cost && wgs < best_wgs) ||
-                            (cost == best_cost && wgs == best_wgs && nw > p.nw) ||
-                            (cost == best_cost && wgs == best_wgs && nw == p.nw && nt * mt > p.nt * p.mtt);
+                            (cost == best_cost && wgs == best_wgs && nt > p.nt) ||
+                            (cost == best_cost && wgs == best_wgs && nt == p.nt && nw > p.nw) ||
+                            (cost == best_cost && wgs == best_wgs && nt == p.nt && nw == p.nw && nt * mt > p.nt * p.mtt);
         if (better) {
           best_cost = cost;
           best_wgs = wgs;
