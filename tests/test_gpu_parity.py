@@ -451,3 +451,56 @@ def test_ragged_with_equal_counts_is_the_uniform_call(rv, gpu):
     for w in range(6):
         np.testing.assert_array_equal(v.output(w).cpu().numpy().reshape(r1[2][w].shape), r1[2][w])
     v.close()
+
+
+@pytest.mark.parametrize("shape,B", [(workload.TINY, 256), (workload.TINY_GQA_BF16, 64)], ids=["tiny-f32", "tiny-bf16"])
+def test_maximum_drafts_and_batch(rv, gpu, shape, B):
+    """k = RV_MAX_DRAFTS drafts for a batch of up to RV_MAX_BATCH sequences
+    (blocks of 1 + 2k + |R| + P = 73 rows), at alpha = 0.3 and 0.  Every
+    sequence's decision must be Algorithm 2 applied to the fused rows the
+    pass itself returns (lowest id on ties).  Sequences 0 and 1 share a
+    history whose drafts are the oracle's greedy continuation (sequence 1's
+    replaced half way), and the last sequence has random drafts; those three
+    are compared with the oracle.  At alpha = 0 (z = o, Eq. 2) all 32 greedy
+    drafts are accepted and the replaced one is rejected."""
+    import torch
+    k, P = rv.RV_MAX_DRAFTS, 4
+    hists = [list(map(int, workload.random_ids(shape.vocab, 24 + b % 17, 31, b))) for b in range(B)]
+    hists[1] = hists[0]
+    drafts = np.stack([workload.random_ids(shape.vocab, k, 31, 7, b) for b in range(B)]).astype(np.int32)
+    past = oracle.prefix_kv(shape, 5, hists[0][:-1])
+    drafts[0] = oracle.greedy_continuation(shape, 5, hists[0], k, past=past)
+    drafts[1] = drafts[0]
+    drafts[1, k // 2] = (drafts[1, k // 2] + 1) % shape.vocab
+    probe = workload.random_ids(shape.vocab, 4, 31, 0xBEEF)
+    S = 1 + 2 * k + len(probe) + P
+    v = rv.Verifier(shape, 5, B, max(len(h) for h in hists) + S + 8, max_block=S, max_drafts=k)
+    got = {}
+    try:
+        lens = v.prefill(hists)
+        for alpha in (0.3, 0.0):
+            acc, nxt = v.verify(lens, drafts, probe, alpha, P)
+            torch.cuda.synchronize()
+            got[alpha] = (acc.cpu().numpy().copy(), nxt.cpu().numpy().copy(), v.output(rv.RV_OUT_FUSED).cpu().numpy())
+    finally:
+        v.close()
+    for alpha, (acc, nxt, z) in got.items():
+        for b in range(B):
+            am = np.argmax(z[b], axis=-1)
+            n = next((i for i in range(k) if am[i] != drafts[b][i]), k)
+            assert (int(acc[b]), int(nxt[b])) == (n, int(am[n])), (alpha, b)
+    for b in (0, 1, B - 1):
+        ref = oracle.verify(shape, 5, hists[b], drafts[b], probe, 0.3, P, past=past if b < 2 else None)
+        acc, nxt, z = got[0.3]
+        logits_close(shape, z[b], ref["z"])
+        if not ref["near_tie"]:
+            assert (int(acc[b]), int(nxt[b])) == (ref["accept_len"], ref["next_id"]), (b, ref["margins"])
+        else:
+            assert greedy_allowed(ref["z"], drafts[b], int(acc[b]), int(nxt[b])), b
+        z0 = oracle.fuse(ref["o"], ref["r"], 0.0).astype(np.float64)
+        n0, t0 = oracle.accept_greedy(z0, drafts[b])
+        acc, nxt, z = got[0.0]
+        logits_close(shape, z[b], z0)
+        if not oracle.decision_margins(z0, drafts[b], n0)[2]:
+            assert (int(acc[b]), int(nxt[b])) == (n0, t0), b
+    assert int(got[0.0][0][0]) == k and int(got[0.0][0][1]) == k // 2
