@@ -120,10 +120,9 @@ inline GemmPlan plan_matmul(bool bf16, bool swiglu, int M, int N, int K, bool al
   p.gk = 1;
   // Many tokens (bf16): the LDS-tiled kernel (one 8- or 12-wave workgroup per CU)
   // streams the weights about once for all token groups.  The shape is
-  // chosen to minimise (rounds of 256 workgroups) x (work per workgroup);
-  // ties go to fewer workgroups, then more rows and tokens per workgroup
-  // (measured over the 8B, 14B and 70B matrices at 172-496 tokens: within
-  // 6% of the best of every shape tried).  K is split only for outputs whose
+  // chosen to minimise (rounds of 256 workgroups) x (work per workgroup),
+  // ties broken as below (measured over the 8B, 14B and 70B matrices at
+  // 172-496 tokens: within 6% of the best of every shape tried).  K is split only for outputs whose
   // consumer adds k-group partials.
   if (bf16 && M > kSplitRows && N % 256 == 0) {
     p.tiled = true;
@@ -136,10 +135,10 @@ inline GemmPlan plan_matmul(bool bf16, bool swiglu, int M, int N, int K, bool al
     // do the same for widths that twelve waves do not divide (14B QKV at
     // 172 tokens: 168 -> 224 workgroups, 39.8 -> 35.3 us).  Equal costs go
     // to fewer workgroups, then more row tiles per wave (each staged operand
-    // tile feeds that many MFMAs, so the LDS reads per MFMA halve from 2 to
-    // 4: O and down as 4 x 4 instead of 2 x 8, 8B batch 16 17.91 -> 17.76
-    // ms, 70B 126.9 -> 124.9 ms), then more waves per workgroup (the 14B
-    // gate/up: 12 waves x 4 tokens tiles 104 us, 8 waves x 6 token tiles
+    // tile feeds that many MFMAs, so 4 row tiles need half the LDS reads per
+    // MFMA of 2: O and down as 4 x 4 instead of 2 x 8, 8B batch 16 17.91 ->
+    // 17.76 ms, 70B 126.9 -> 124.9 ms), then more waves per workgroup (the
+    // 14B gate/up: 12 waves x 4 token tiles 104 us, 8 waves x 6 token tiles
     // 108 us), then larger tiles.
     const int shapes[][3] = {{8, 4, 8}, {8, 2, 8}, {8, 4, 4}, {8, 2, 4}, {12, 2, 4}, {8, 2, 6}};
     for (const auto& sh : shapes) {
