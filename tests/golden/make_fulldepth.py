@@ -43,7 +43,7 @@ import workload  # noqa: E402
 # second).
 PLAN = {
     "8b-bf16-b1": [(0, "all", "workload"), (1, "all", "workload"), (0, "all", "greedy")],
-    "8b-bf16-b16-ragged": [(0, "short+long", "workload")],
+    "8b-bf16-b16-ragged": [(0, "short+long", "workload"), (0, [8], "greedy")],
     "14b-bf16-b4": [(0, [0, 3], "workload"), (0, [0], "greedy")],
     "70b-bf16-b8": [(0, [5], "workload"), (0, [5], "greedy")],
 }
