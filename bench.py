@@ -176,7 +176,7 @@ def stored_parity(rv, v, w, lens, drafts):
         return None
     with open(path) as f:
         fx = json.load(f)
-    case = next((c for c in fx["cases"] if c["case"] == 0), None)
+    case = next((c for c in fx["cases"] if c["case"] == 0 and c.get("drafts_rule", "workload") == "workload"), None)
     if case is None or case["prefix_len"] != list(lens):
         return None
     acc = v.accept_len.cpu().numpy()
