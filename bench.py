@@ -278,8 +278,9 @@ def main():
                     help="time the end-to-end speculative loop (1B-shaped draft + 8B-shaped target) instead")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (the verify pass shards by sequence "
-              "across data-parallel replicas; see the design notes). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (the verify pass would shard by "
+              "sequence across data-parallel replicas, with no communication inside a pass). Run with --gpus 1.",
+              file=sys.stderr)
         sys.exit(2)
 
     if args.calibrate_copy:
